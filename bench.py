@@ -1,0 +1,164 @@
+"""Benchmark of the rk-Rotor solve on one MI355X.
+
+One step is one pass of the whole hot path over one chain: the table fill for
+every span and every budget (App. C, Alg. 2), the answer read-back, and the
+schedule (Alg. 3) copied to the host.  The chain is the deep transformer-like
+workload, 384 blocks with 16 options each at a 6000-slot budget, created and
+uploaded before the timed region; the table lives in a torch allocation and
+the solve runs on a torch stream.
+
+Prints one JSON line on stdout.  ``value`` is DP relaxations per second of
+the whole step (relaxations = candidate evaluations of the recurrence,
+(M+1) * sum_d (L-d)(K+d)).  ``roofline`` reports the dominant fill kernel
+against the VALU integer peak, from per-launch HIP events on the solve's
+stream.  ``cpu_baseline`` times the CPU oracle (one core) on a bounded part of
+the same chain.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "DP relaxations/sec + wall solve time per chain on 1 MI355X; % HBM/VALU roofline"
+WORKLOAD_CFG = 4
+# MI355X: 256 CUs x 4 SIMD16 = 64 int32 lanes per CU per clock at 2.4 GHz
+VALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
+OPS_PER_RELAX = 2  # one add and one min per candidate
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(ch, nblocks: int):
+    import oracle
+    from paper_2307_01236_amd.chaingen import relaxations
+    if not os.path.exists(oracle.LIB):
+        oracle.build(force=False)
+    sub = ch.sub(0, nblocks - 1)
+    t0 = time.perf_counter()
+    oracle.solve(sub)
+    dt = time.perf_counter() - t0
+    r = relaxations(sub.L, sub.K, sub.M)
+    return {"value": r / dt, "unit": "relaxations/s", "cores": 1, "kind": "oracle",
+            "sample": f"blocks 0..{nblocks - 1} of the same chain, M={sub.M}: {r:.3e} relaxations "
+                      f"in {dt:.2f} s on one host core",
+            "seconds": dt}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=WORKLOAD_CFG)
+    ap.add_argument("--cpu-blocks", type=int, default=96, help="oracle sample size (0: skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: the solver runs on a single MI355X and this build "
+              f"has no multi-GPU path (asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2307_01236_amd import rk
+    from paper_2307_01236_amd.chaingen import CONFIGS, cells, make_config_chain, relaxations
+
+    torch.cuda.set_device(0)
+    ch = make_config_chain(args.config)
+    M = ch.M
+    relax = relaxations(ch.L, ch.K, M)
+    ncells = cells(ch.L, M)
+    log(f"workload {ch.name}: L={ch.L} K={ch.K} M={M} relaxations={relax:.3e} sha={ch.sha256()[:16]}")
+
+    s = rk.Solver(ch)
+    nbytes = s.workspace_bytes(M)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+    stream = torch.cuda.Stream()
+    s.set_profiling(True)
+
+    def step():
+        s.solve_async(M, ws.data_ptr(), nbytes, stream.cuda_stream)
+        ans = s.result()
+        ops, _ = s.schedule()
+        return ans, len(ops)
+
+    for i in range(args.warmup):
+        ans, nops = step()
+        log(f"warmup {i}: answer={ans} ops={nops}")
+
+    fill_ms, kern = [], {}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ans, nops = step()
+        fm, _ = s.fill_ms()
+        fill_ms.append(fm)
+        for name, (n, ms) in s.kernel_stats().items():
+            a = kern.setdefault(name, [0, 0.0])
+            a[0] += n
+            a[1] += ms
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, fill median {statistics.median(fill_ms):.3f} ms")
+
+    # solve wall time without the schedule, warm (synchronous rk_solve on the library's table)
+    wall = []
+    for _ in range(3):
+        t = time.perf_counter()
+        s.solve(M)
+        wall.append((time.perf_counter() - t) * 1e3)
+    t = time.perf_counter()
+    s.schedule()
+    sched_ms = (time.perf_counter() - t) * 1e3
+
+    dom = max(kern.items(), key=lambda kv: kv[1][1])
+    dname, (dn, dms) = dom
+    per_launch_ms = dms / dn
+    relax_per_launch = relax * args.steps / dn if len(kern) == 1 else None
+    achieved_tops = OPS_PER_RELAX * relax * args.steps / (dms * 1e-3) / 1e12 if len(kern) == 1 else None
+    roofline = {
+        "bound": "alu", "kernel": dname,
+        "achieved": achieved_tops, "peak": VALU_PEAK_TOPS, "unit": "TOP/s",
+        "frac": (achieved_tops / VALU_PEAK_TOPS) if achieved_tops else None,
+        "traffic": None,
+        "launches_per_step": dn / args.steps, "avg_launch_ms": per_launch_ms,
+        "ops_per_launch": OPS_PER_RELAX * relax_per_launch if relax_per_launch else None,
+    }
+
+    cpu = None
+    if args.cpu_blocks > 0:
+        log(f"cpu baseline: oracle on {args.cpu_blocks} blocks ...")
+        cpu = cpu_baseline(ch, min(args.cpu_blocks, ch.L))
+        log(f"cpu baseline: {cpu['value']:.3e} relax/s ({cpu['seconds']:.1f} s)")
+
+    out = {
+        "metric": METRIC, "value": relax / (ms_per_step * 1e-3), "unit": "relaxations/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int32",
+        "data": "synthetic",
+        "config": {"workload": ch.name, "L": ch.L, "K": ch.K, "M": M, "relaxations": relax,
+                   "cells": ncells, "chain_sha256": ch.sha256(), "answer": ans, "schedule_ops": nops},
+        "wall_solve_ms": statistics.median(wall), "fill_ms": statistics.median(fill_ms),
+        "schedule_ms": sched_ms,
+        "fill_relax_per_s": relax / (statistics.median(fill_ms) * 1e-3),
+        "roofline": roofline, "cpu_baseline": cpu,
+        "kernels": {k: {"launches_per_step": v[0] / args.steps, "ms_per_step": v[1] / args.steps}
+                    for k, v in kern.items()},
+    }
+    s.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,161 @@
+/*
+ * rk.h -- C ABI of librkrotor, the rk-Rotor solver of Rockmate (arXiv 2307.01236)
+ * on AMD Instinct MI355X (gfx950).
+ *
+ * The library computes rk-Rotor's dynamic program (App. C, Eqs. fe, fn and
+ * all; Alg. 2) on the GPU and turns its optimum into a compute/forget
+ * schedule (Alg. 3).  It plays the role of the line of Rockmate's Alg. 1 that
+ * produces Sequence = rk-Rotor(sols, M_GPU): the per-block option sets come in
+ * through rk_chain_create, the budget through rk_solve, and the schedule
+ * comes out of rk_extract_schedule.
+ *
+ * Model (App. C notation, 0-based):
+ *   - blocks 0..L-1; activation x_i is the input of block i, x_L the output;
+ *   - F_i^0 is the forward that keeps nothing: time r(F_i^0) = fn_time[i],
+ *     temporary memory tmp(F_i^0) = fn_tmp[i];
+ *   - each block has K saving options o = 0..K-1: forward F_i^o (time
+ *     fwd[i*K+o], temporary tmp_fwd[i*K+o]) which keeps mem[i*K+o] slots of
+ *     intermediates until the backward B_i^o (time bwd[i*K+o], temporary
+ *     tmp_bwd[i*K+o]).  The paper's xbar_i^o is x_{i+1} + mem[i*K+o];
+ *   - Opt(s,t,m) is the best time for blocks s..t (inclusive) when x_s stays
+ *     live and m slots are available beyond it; the answer for a budget M is
+ *     Opt(0, L-1, M - x_0);
+ *   - sizes, budgets and times are non-negative integers (memory "slots" and
+ *     time units of the caller's choosing); all arithmetic is exact.
+ *
+ * Ties: when several choices reach the optimum the one recorded is the
+ * lexicographic minimum of (cost, code) with code = i for the case-2 split
+ * that keeps x_i and code = L + o for the case-1 option o (Alg. 3 tests case 2
+ * before case 1; smaller i, then smaller o).  This makes every table and
+ * schedule unique.
+ *
+ * Threading: a chain is not thread-safe; distinct chains are independent.
+ * Device: the library works on the HIP device current at the first solve of
+ * a chain and keeps using it for that chain.
+ * Errors: every call returns an RK_* code; nothing is thrown across the ABI.
+ */
+#ifndef RK_H
+#define RK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RK_INF INT32_MAX                  /* "no valid schedule" (Eq. all: +infinity)    */
+#define RK_TIME_LIMIT ((int32_t)((1 << 30) - 2)) /* largest admissible schedule-time bound */
+#define RK_MAX_L 2000                     /* longest chain                                */
+#define RK_MAX_M ((int32_t)((1 << 26) - 2))       /* largest budget                       */
+
+enum { RK_FWD_NOSAVE = 0, RK_FWD_SAVE = 1, RK_BWD = 2, RK_FREE_X = 3 };
+
+enum {
+    RK_OK = 0,
+    RK_E_INVAL = -1,       /* bad argument (NULL, negative, out of range)                    */
+    RK_E_OVERFLOW = -2,    /* schedule times could exceed RK_TIME_LIMIT                       */
+    RK_E_NOMEM = -3,       /* device or host allocation failed, or workspace too small        */
+    RK_E_DEVICE = -4,      /* a HIP call failed (no device, launch error, ...)                */
+    RK_E_NOT_SOLVED = -5,  /* no completed solve to read from                                 */
+    RK_E_INFEASIBLE = -6,  /* the budget admits no schedule                                   */
+    RK_E_BUFSZ = -7,       /* caller buffer too small; the needed size was returned           */
+    RK_E_INTERNAL = -8     /* a consistency check inside the library failed                    */
+};
+
+/* One schedule step.  kind: RK_FWD_NOSAVE (F_block^0), RK_FWD_SAVE (F_block^option),
+ * RK_BWD (B_block^option), RK_FREE_X (drop activation x_block).  option is -1 for
+ * RK_FWD_NOSAVE and RK_FREE_X. */
+typedef struct { int32_t kind, block, option; } rk_op;
+
+typedef struct rk_chain rk_chain;
+
+/*
+ * Create a chain from its per-block option sets (Alg. 1: the sols of every
+ * block; App. C notation).  All arrays are host memory and are deep-copied,
+ * so the caller may free them on return.  Layouts: x [L+1]; fn_time, fn_tmp
+ * [L]; fwd, bwd, mem, tmp_fwd, tmp_bwd [L*K] row-major (option fastest).
+ * Checks: 1 <= L <= RK_MAX_L, K >= 1, L + K < 32768, every entry >= 0, and the
+ * bound on any schedule's time, L * sum_i max(fn_time_i, max_o fwd_i^o) +
+ * sum_i max_o bwd_i^o, must not exceed RK_TIME_LIMIT (else RK_E_OVERFLOW).
+ * Does not touch the GPU.  On success *out owns a new chain.
+ */
+int rk_chain_create(int32_t L, int32_t K, const int32_t *x, const int32_t *fn_time,
+                    const int32_t *fn_tmp, const int32_t *fwd, const int32_t *bwd,
+                    const int32_t *mem, const int32_t *tmp_fwd, const int32_t *tmp_bwd,
+                    rk_chain **out);
+
+/* Release the chain, its device copies and any table it allocated.  NULL is a no-op. */
+void rk_chain_destroy(rk_chain *c);
+
+/* Bytes of device workspace a solve of this chain at budget M needs (the
+ * Opt table and its companions).  RK_E_INVAL for M outside [0, RK_MAX_M]. */
+int rk_workspace_bytes(const rk_chain *c, int32_t M, size_t *bytes);
+
+/*
+ * Fill Opt(s,t,m) for every span and every m in [0, M] (Alg. 2) in a table
+ * the chain allocates (and reuses across solves), then return the answer
+ * Opt(0, L-1, M - x_0) in *opt_out, or RK_INF when the budget admits no
+ * schedule (including M < x_0).  Synchronous; runs on the null stream.
+ * RK_E_NOMEM if the table cannot be allocated, RK_E_DEVICE on a HIP error.
+ */
+int rk_solve(rk_chain *c, int32_t M, int32_t *opt_out);
+
+/*
+ * Same fill, asynchronous, in caller memory: d_workspace is device memory of
+ * at least rk_workspace_bytes(c, M) bytes (for instance a torch tensor) and
+ * stream a hipStream_t (NULL: the null stream).  Returns once the work is
+ * queued.  The workspace must stay allocated and untouched until the chain is
+ * destroyed or solved again; the chain reads results from it.  Call
+ * rk_result to wait and read the answer.
+ */
+int rk_solve_async(rk_chain *c, int32_t M, void *d_workspace, size_t ws_bytes, void *stream);
+
+/* Wait for the last solve of the chain and return its answer (as rk_solve). */
+int rk_result(rk_chain *c, int32_t *opt_out);
+
+/*
+ * Alg. 3 (rk-Rotor-Build) for the last solve's budget: the schedule as a list
+ * of steps, with every forget of an activation made explicit.  The choice at
+ * each visited (s,t,m) is recomputed on the GPU from the finished Opt table
+ * (the lexicographic (cost, code) minimum).  Two-call: with ops == NULL or
+ * cap smaller than the schedule, *n_ops receives its length and RK_E_BUFSZ is
+ * returned.  *n_fwd (may be NULL) receives the index of the first backward,
+ * i.e. the split between Sequence.fwd and Sequence.bwd.  RK_E_NOT_SOLVED
+ * before a solve, RK_E_INFEASIBLE when the answer is RK_INF.
+ */
+int rk_extract_schedule(rk_chain *c, rk_op *ops, int64_t cap, int64_t *n_ops, int64_t *n_fwd);
+
+/*
+ * Copy row (s,t) of the last solve: opt_row[m] = Opt(s,t,m) (RK_INF where
+ * infeasible) and arg_row[m] = the recorded choice code (-1 where infeasible),
+ * for m = 0..M; each buffer holds M+1 entries and either may be NULL.
+ * RK_E_INVAL unless 0 <= s <= t < L.
+ */
+int rk_read_row(rk_chain *c, int32_t s, int32_t t, int32_t *opt_row, int16_t *arg_row);
+
+/*
+ * Device time of the last solve's table fill, in milliseconds (HIP events
+ * around the fill on the solve's stream), and the number of kernels launched.
+ */
+int rk_last_fill_ms(rk_chain *c, float *ms, int32_t *launches);
+
+/*
+ * Kernel-level timing (for benchmarks; off by default).  While enabled, every
+ * kernel the fill launches is bracketed by a pair of HIP events on the solve's
+ * stream.  rk_fill_kernel_stats then reports, for kernel kind `kind`
+ * (0 <= kind < *n_kinds), its name as a profiler shows it, the number of its
+ * launches in the last solve and their summed device time in milliseconds.
+ * Waits for the last solve.  RK_E_INVAL for a kind out of range.
+ */
+int rk_set_profiling(rk_chain *c, int32_t enable);
+int rk_fill_kernel_stats(rk_chain *c, int32_t kind, int32_t *n_kinds, const char **name,
+                         int32_t *launches, float *total_ms);
+
+/* Short English description of an RK_* code. */
+const char *rk_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* RK_H */

@@ -1,0 +1,410 @@
+// rk_api.hip -- the C ABI of librkrotor (declared in include/rk.h).
+//
+// Host side: argument checks, the per-chain precompute of App. C's derived
+// quantities, device buffers, kernel launches and read-back.  No step of the
+// dynamic program itself runs here; the fill, the choice recovery and Alg. 3
+// all run in the kernels of rk_kernels.hip.
+#include <algorithm>
+#include <new>
+#include <vector>
+
+#include "rk_internal.h"
+
+using rk::DevChain;
+using rk::DINF;
+
+struct rk_chain {
+    int32_t L = 0, K = 0;
+    std::vector<int32_t> x, xbar, c1, need1, P, need2;  // host copies of the device arrays
+
+    int device = -1;
+    void *d_chain = nullptr;  // x | xbar | c1 | need1 | P | need2
+    DevChain dc{};
+
+    void *own_ws = nullptr;  // table owned by the chain (rk_solve)
+    size_t own_ws_bytes = 0;
+    int32_t *tab = nullptr;  // table of the last solve (own or caller's)
+    hipStream_t stream = nullptr;
+    int32_t M = -1, W = 0, stride = 0;
+    bool queued = false;
+
+    hipEvent_t ev_fill0 = nullptr, ev_fill1 = nullptr;
+    int32_t launches = 0;
+    rk::Profiler prof;
+
+    rk_op *d_ops = nullptr;  // backtrace output
+    int64_t d_ops_cap = 0;
+    int64_t *d_res = nullptr;
+    int16_t *d_argrow = nullptr;
+    int32_t d_argrow_cap = 0;
+};
+
+namespace {
+
+constexpr int64_t kSizeCap = int64_t(1) << 30;  // derived sizes saturate here (above any budget)
+
+#define HIPCHK(expr)                                    \
+    do {                                                \
+        if ((expr) != hipSuccess) return RK_E_DEVICE;   \
+    } while (0)
+
+// Runs on the chain's device, restoring the caller's current device afterwards.
+struct DeviceScope {
+    int prev = -1;
+    bool ok = true;
+    explicit DeviceScope(rk_chain *c)
+    {
+        if (hipGetDevice(&prev) != hipSuccess) { ok = false; return; }
+        if (c->device < 0) c->device = prev;
+        else if (c->device != prev && hipSetDevice(c->device) != hipSuccess) ok = false;
+    }
+    ~DeviceScope()
+    {
+        int cur = -1;
+        if (ok && hipGetDevice(&cur) == hipSuccess && cur != prev && prev >= 0) (void)hipSetDevice(prev);
+    }
+};
+
+int table_bytes(int32_t L, int32_t M, size_t *bytes)
+{
+    if (M < 0 || M > RK_MAX_M) return RK_E_INVAL;
+    const int64_t rows = rk::n_rows(L);
+    const int64_t stride = rk::row_stride(M + 1);
+    const int64_t elems = rows * stride;
+    if (elems <= 0 || elems > (int64_t(1) << 40)) return RK_E_NOMEM;
+    *bytes = (size_t)elems * sizeof(int32_t);
+    return RK_OK;
+}
+
+// First solve on a device: upload the derived arrays and create the events.
+int ensure_device(rk_chain *c)
+{
+    if (c->d_chain) return RK_OK;
+    const int32_t L = c->L, K = c->K;
+    const size_t nx = L + 1, nk = (size_t)L * K, nl = (size_t)L * L;
+    const size_t total = nx + 3 * nk + 2 * nl;
+    HIPCHK(hipMalloc(&c->d_chain, total * sizeof(int32_t)));
+    int32_t *p = static_cast<int32_t *>(c->d_chain);
+    size_t off = 0;
+    auto put = [&](const std::vector<int32_t> &v) -> const int32_t * {
+        int32_t *dst = p + off;
+        off += v.size();
+        return hipMemcpy(dst, v.data(), v.size() * sizeof(int32_t), hipMemcpyHostToDevice) == hipSuccess
+                   ? dst
+                   : nullptr;
+    };
+    c->dc.L = L;
+    c->dc.K = K;
+    c->dc.x = put(c->x);
+    c->dc.xbar = put(c->xbar);
+    c->dc.c1 = put(c->c1);
+    c->dc.need1 = put(c->need1);
+    c->dc.P = put(c->P);
+    c->dc.need2 = put(c->need2);
+    if (!c->dc.x || !c->dc.xbar || !c->dc.c1 || !c->dc.need1 || !c->dc.P || !c->dc.need2)
+        return RK_E_DEVICE;
+    HIPCHK(hipEventCreate(&c->ev_fill0));
+    HIPCHK(hipEventCreate(&c->ev_fill1));
+    HIPCHK(hipMalloc(&c->d_res, 4 * sizeof(int64_t)));
+    return RK_OK;
+}
+
+int32_t to_abi(int32_t v) { return v >= DINF ? RK_INF : v; }
+
+int fill(rk_chain *c, int32_t M, int32_t *tab, hipStream_t stream)
+{
+    c->queued = false;
+    c->M = M;
+    c->W = M + 1;
+    c->stride = rk::row_stride(c->W);
+    c->tab = tab;
+    c->stream = stream;
+    c->prof.reset(stream);
+    HIPCHK(hipEventRecord(c->ev_fill0, stream));
+    HIPCHK(rk::launch_fill(c->dc, tab, c->W, c->stride, stream, &c->launches, &c->prof));
+    HIPCHK(hipEventRecord(c->ev_fill1, stream));
+    c->queued = true;
+    return RK_OK;
+}
+
+int answer(rk_chain *c, int32_t *out)
+{
+    if (!c->queued) return RK_E_NOT_SOLVED;
+    HIPCHK(hipEventSynchronize(c->ev_fill1));
+    if (c->M < c->x[0]) { *out = RK_INF; return RK_OK; }
+    int32_t v = 0;
+    const int64_t idx = rk::row_of(c->L, 0, c->L - 1) * c->stride + (c->M - c->x[0]);
+    HIPCHK(hipMemcpy(&v, c->tab + idx, sizeof(int32_t), hipMemcpyDeviceToHost));
+    *out = to_abi(v);
+    return RK_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int rk_chain_create(int32_t L, int32_t K, const int32_t *x, const int32_t *fn_time,
+                    const int32_t *fn_tmp, const int32_t *fwd, const int32_t *bwd,
+                    const int32_t *mem, const int32_t *tmp_fwd, const int32_t *tmp_bwd,
+                    rk_chain **out)
+{
+    if (!out) return RK_E_INVAL;
+    *out = nullptr;
+    if (L < 1 || L > RK_MAX_L || K < 1 || (int64_t)L + K >= 32768) return RK_E_INVAL;
+    if (!x || !fn_time || !fn_tmp || !fwd || !bwd || !mem || !tmp_fwd || !tmp_bwd) return RK_E_INVAL;
+    const int64_t nk = (int64_t)L * K;
+    for (int32_t i = 0; i <= L; ++i)
+        if (x[i] < 0) return RK_E_INVAL;
+    for (int32_t i = 0; i < L; ++i)
+        if (fn_time[i] < 0 || fn_tmp[i] < 0) return RK_E_INVAL;
+    for (int64_t j = 0; j < nk; ++j)
+        if (fwd[j] < 0 || bwd[j] < 0 || mem[j] < 0 || tmp_fwd[j] < 0 || tmp_bwd[j] < 0)
+            return RK_E_INVAL;
+    // Bound on any schedule's time: a block is forwarded at most L times, backwarded once.
+    int64_t fsum = 0, bsum = 0;
+    for (int32_t i = 0; i < L; ++i) {
+        int64_t fm = fn_time[i], bm = 0;
+        for (int32_t o = 0; o < K; ++o) {
+            fm = std::max<int64_t>(fm, fwd[(int64_t)i * K + o]);
+            bm = std::max<int64_t>(bm, bwd[(int64_t)i * K + o]);
+        }
+        fsum += fm;
+        bsum += bm;
+    }
+    if ((int64_t)L * fsum + bsum > RK_TIME_LIMIT) return RK_E_OVERFLOW;
+
+    rk_chain *c = new (std::nothrow) rk_chain;
+    if (!c) return RK_E_NOMEM;
+    try {
+        c->L = L;
+        c->K = K;
+        c->x.assign(x, x + L + 1);
+        c->xbar.resize(nk);
+        c->c1.resize(nk);
+        c->need1.resize(nk);
+        c->P.assign((size_t)L * L, 0);
+        c->need2.assign((size_t)L * L, 0);
+    } catch (...) {
+        delete c;
+        return RK_E_NOMEM;
+    }
+    // Case 1 (Eq. fe): F_s^o leaves xbar = x_{s+1} + mem live; it and B_s^o need their
+    // temporary memory on top of that; the pair costs r(F_s^o) + r(B_s^o).
+    for (int32_t s = 0; s < L; ++s)
+        for (int32_t o = 0; o < K; ++o) {
+            const int64_t j = (int64_t)s * K + o;
+            const int64_t xb = (int64_t)x[s + 1] + mem[j];
+            c->xbar[j] = (int32_t)std::min(xb, kSizeCap);
+            c->need1[j] = (int32_t)std::min(xb + std::max(tmp_fwd[j], tmp_bwd[j]), kSizeCap);
+            c->c1[j] = fwd[j] + bwd[j];
+        }
+    // Case 2 (Eq. fn): the sweep F_s^0..F_{i-1}^0 costs P[s][i]; F_k^0 holds its input
+    // (except the span input x_s, outside the budget), its output and tmp(F_k^0).
+    for (int32_t s = 0; s < L; ++s) {
+        int64_t p = 0, need = 0;
+        for (int32_t i = s + 1; i < L; ++i) {
+            const int32_t k = i - 1;
+            p += fn_time[k];
+            need = std::max<int64_t>(need, (k > s ? (int64_t)x[k] : 0) + x[k + 1] + fn_tmp[k]);
+            c->P[(size_t)s * L + i] = (int32_t)p;
+            c->need2[(size_t)s * L + i] = (int32_t)std::min(need, kSizeCap);
+        }
+    }
+    *out = c;
+    return RK_OK;
+}
+
+void rk_chain_destroy(rk_chain *c)
+{
+    if (!c) return;
+    if (c->d_chain) {
+        DeviceScope ds(c);
+        if (c->queued && c->ev_fill1) (void)hipEventSynchronize(c->ev_fill1);
+        (void)hipFree(c->d_chain);
+        if (c->own_ws) (void)hipFree(c->own_ws);
+        if (c->d_ops) (void)hipFree(c->d_ops);
+        if (c->d_res) (void)hipFree(c->d_res);
+        if (c->d_argrow) (void)hipFree(c->d_argrow);
+        if (c->ev_fill0) (void)hipEventDestroy(c->ev_fill0);
+        if (c->ev_fill1) (void)hipEventDestroy(c->ev_fill1);
+        for (hipEvent_t e : c->prof.events) (void)hipEventDestroy(e);
+    }
+    delete c;
+}
+
+int rk_workspace_bytes(const rk_chain *c, int32_t M, size_t *bytes)
+{
+    if (!c || !bytes) return RK_E_INVAL;
+    return table_bytes(c->L, M, bytes);
+}
+
+int rk_solve_async(rk_chain *c, int32_t M, void *d_workspace, size_t ws_bytes, void *stream)
+{
+    if (!c) return RK_E_INVAL;
+    size_t need = 0;
+    int rc = table_bytes(c->L, M, &need);
+    if (rc != RK_OK) return rc;
+    DeviceScope ds(c);
+    if (!ds.ok) return RK_E_DEVICE;
+    if ((rc = ensure_device(c)) != RK_OK) return rc;
+    if (c->queued) HIPCHK(hipEventSynchronize(c->ev_fill1));  // previous fill may still read its table
+    int32_t *tab;
+    if (d_workspace) {
+        if (ws_bytes < need) return RK_E_NOMEM;
+        tab = static_cast<int32_t *>(d_workspace);
+    } else {
+        if (c->own_ws_bytes < need) {
+            if (c->own_ws) HIPCHK(hipFree(c->own_ws));
+            c->own_ws = nullptr;
+            c->own_ws_bytes = 0;
+            if (hipMalloc(&c->own_ws, need) != hipSuccess) {
+                (void)hipGetLastError();
+                c->queued = false;
+                return RK_E_NOMEM;
+            }
+            c->own_ws_bytes = need;
+        }
+        tab = static_cast<int32_t *>(c->own_ws);
+    }
+    return fill(c, M, tab, static_cast<hipStream_t>(stream));
+}
+
+int rk_solve(rk_chain *c, int32_t M, int32_t *opt_out)
+{
+    if (!c || !opt_out) return RK_E_INVAL;
+    int rc = rk_solve_async(c, M, nullptr, 0, nullptr);
+    if (rc != RK_OK) return rc;
+    DeviceScope ds(c);
+    return answer(c, opt_out);
+}
+
+int rk_result(rk_chain *c, int32_t *opt_out)
+{
+    if (!c || !opt_out) return RK_E_INVAL;
+    if (!c->queued) return RK_E_NOT_SOLVED;
+    DeviceScope ds(c);
+    if (!ds.ok) return RK_E_DEVICE;
+    return answer(c, opt_out);
+}
+
+int rk_extract_schedule(rk_chain *c, rk_op *ops, int64_t cap, int64_t *n_ops, int64_t *n_fwd)
+{
+    if (!c || !n_ops || cap < 0) return RK_E_INVAL;
+    if (!c->queued) return RK_E_NOT_SOLVED;
+    DeviceScope ds(c);
+    if (!ds.ok) return RK_E_DEVICE;
+    int32_t ans = 0;
+    int rc = answer(c, &ans);
+    if (rc != RK_OK) return rc;
+    if (ans == RK_INF) return RK_E_INFEASIBLE;
+    // At most L forwards per block (one saving) and one backward, one forget per no-save forward.
+    const int64_t max_ops = 2 * (int64_t)c->L * c->L + 16;
+    if (c->d_ops_cap < max_ops) {
+        if (c->d_ops) HIPCHK(hipFree(c->d_ops));
+        c->d_ops = nullptr;
+        c->d_ops_cap = 0;
+        if (hipMalloc(&c->d_ops, max_ops * sizeof(rk_op)) != hipSuccess) return RK_E_NOMEM;
+        c->d_ops_cap = max_ops;
+    }
+    HIPCHK(rk::launch_backtrace(c->dc, c->tab, c->stride, c->M - c->x[0], c->d_ops, c->d_ops_cap,
+                                c->d_res, c->stream));
+    int64_t res[3] = {0, 0, 0};
+    HIPCHK(hipMemcpyAsync(res, c->d_res, sizeof(res), hipMemcpyDeviceToHost, c->stream));
+    HIPCHK(hipStreamSynchronize(c->stream));
+    if (res[2] != 0 || res[0] > c->d_ops_cap) return RK_E_INTERNAL;
+    *n_ops = res[0];
+    if (n_fwd) *n_fwd = res[1];
+    if (!ops || cap < res[0]) return RK_E_BUFSZ;
+    HIPCHK(hipMemcpy(ops, c->d_ops, res[0] * sizeof(rk_op), hipMemcpyDeviceToHost));
+    return RK_OK;
+}
+
+int rk_read_row(rk_chain *c, int32_t s, int32_t t, int32_t *opt_row, int16_t *arg_row)
+{
+    if (!c || s < 0 || t < s || t >= c->L) return RK_E_INVAL;
+    if (!c->queued) return RK_E_NOT_SOLVED;
+    DeviceScope ds(c);
+    if (!ds.ok) return RK_E_DEVICE;
+    HIPCHK(hipEventSynchronize(c->ev_fill1));
+    const int64_t base = rk::row_of(c->L, s, t) * c->stride;
+    if (opt_row) {
+        HIPCHK(hipMemcpy(opt_row, c->tab + base, (size_t)c->W * sizeof(int32_t), hipMemcpyDeviceToHost));
+        for (int32_t m = 0; m < c->W; ++m) opt_row[m] = to_abi(opt_row[m]);
+    }
+    if (arg_row) {
+        if (c->d_argrow_cap < c->W) {
+            if (c->d_argrow) HIPCHK(hipFree(c->d_argrow));
+            c->d_argrow = nullptr;
+            c->d_argrow_cap = 0;
+            if (hipMalloc(&c->d_argrow, (size_t)c->W * sizeof(int16_t)) != hipSuccess) return RK_E_NOMEM;
+            c->d_argrow_cap = c->W;
+        }
+        HIPCHK(rk::launch_arg_row(c->dc, c->tab, c->W, c->stride, s, t, c->d_argrow, c->stream));
+        HIPCHK(hipMemcpyAsync(arg_row, c->d_argrow, (size_t)c->W * sizeof(int16_t),
+                              hipMemcpyDeviceToHost, c->stream));
+        HIPCHK(hipStreamSynchronize(c->stream));
+    }
+    return RK_OK;
+}
+
+int rk_last_fill_ms(rk_chain *c, float *ms, int32_t *launches)
+{
+    if (!c || !ms) return RK_E_INVAL;
+    if (!c->queued) return RK_E_NOT_SOLVED;
+    DeviceScope ds(c);
+    if (!ds.ok) return RK_E_DEVICE;
+    HIPCHK(hipEventSynchronize(c->ev_fill1));
+    HIPCHK(hipEventElapsedTime(ms, c->ev_fill0, c->ev_fill1));
+    if (launches) *launches = c->launches;
+    return RK_OK;
+}
+
+int rk_set_profiling(rk_chain *c, int32_t enable)
+{
+    if (!c) return RK_E_INVAL;
+    c->prof.on = enable != 0;
+    return RK_OK;
+}
+
+int rk_fill_kernel_stats(rk_chain *c, int32_t kind, int32_t *n_kinds, const char **name,
+                         int32_t *launches, float *total_ms)
+{
+    if (!c) return RK_E_INVAL;
+    if (n_kinds) *n_kinds = rk::KFILL_NKINDS;
+    if (kind < 0 || kind >= rk::KFILL_NKINDS) return RK_E_INVAL;
+    if (name) *name = rk::kFillKernelNames[kind];
+    if (!c->queued) return RK_E_NOT_SOLVED;
+    DeviceScope ds(c);
+    if (!ds.ok) return RK_E_DEVICE;
+    HIPCHK(hipEventSynchronize(c->ev_fill1));
+    int32_t cnt = 0;
+    float sum = 0.f;
+    for (int32_t j = 0; j < c->prof.n; ++j) {
+        if (c->prof.kinds[j] != kind) continue;
+        float ms = 0.f;
+        HIPCHK(hipEventElapsedTime(&ms, c->prof.events[2 * j], c->prof.events[2 * j + 1]));
+        sum += ms;
+        ++cnt;
+    }
+    if (launches) *launches = cnt;
+    if (total_ms) *total_ms = sum;
+    return RK_OK;
+}
+
+const char *rk_strerror(int code)
+{
+    switch (code) {
+    case RK_OK: return "ok";
+    case RK_E_INVAL: return "invalid argument";
+    case RK_E_OVERFLOW: return "schedule times could exceed RK_TIME_LIMIT";
+    case RK_E_NOMEM: return "allocation failed or workspace too small";
+    case RK_E_DEVICE: return "HIP device error";
+    case RK_E_NOT_SOLVED: return "no solve to read from";
+    case RK_E_INFEASIBLE: return "budget admits no schedule";
+    case RK_E_BUFSZ: return "buffer too small";
+    case RK_E_INTERNAL: return "internal consistency check failed";
+    default: return "unknown error";
+    }
+}
+
+}  // extern "C"

@@ -1,0 +1,212 @@
+"""Parity of the HIP path with the CPU oracle (MI355X).
+
+Every value compared here comes from the C ABI (librkrotor through its thin
+binding) on one side and from the oracle on the other; both get the same
+seeded chains.  Opt tables, recorded choices and schedules must match exactly:
+all costs are integers.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2307_01236_amd import rk
+from paper_2307_01236_amd.chaingen import (CONFIGS, make_config_chain, make_random_chain,
+                                            store_all_bound)
+
+pytestmark = pytest.mark.gpu
+INF = rk.RK_INF
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def full_parity(ch, M=None, check_schedule=True):
+    """Whole Opt and choice tables, the answer and the schedule."""
+    M = ch.M if M is None else M
+    say(f"  full parity {ch.name} L={ch.L} K={ch.K} M={M}")
+    sol = oracle.solve(ch, M)
+    s = rk.Solver(ch)
+    try:
+        ans = s.solve(M)
+        assert ans == sol.answer, (ans, sol.answer)
+        g_opt, g_arg = s.rows()
+        o_opt, o_arg = sol.rows()
+        bad = np.argwhere(g_opt != o_opt)
+        assert bad.size == 0, f"Opt differs at {len(bad)} cells, first {bad[:3].tolist()}"
+        bad = np.argwhere(g_arg != o_arg)
+        assert bad.size == 0, f"choice differs at {len(bad)} cells, first {bad[:3].tolist()}"
+        if check_schedule:
+            check_same_schedule(s, sol, ch, M)
+    finally:
+        s.close()
+    return sol
+
+
+def check_same_schedule(s, sol, ch, M):
+    exp = oracle.schedule(sol, M)
+    if exp is None:
+        with pytest.raises(rk.RKError) as e:
+            s.schedule()
+        assert e.value.code == rk.RK_E_INFEASIBLE
+        return
+    ops, nfwd = s.schedule()
+    assert np.array_equal(ops, exp[0]) and nfwd == exp[1]
+    ok, tm, pk, _ = oracle.simulate(ch, ops)
+    assert ok and tm == sol.answer and pk <= M
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2])
+def test_configs_full_tables(cfg):
+    for rep in range(2 if cfg < 2 else 1):
+        full_parity(make_config_chain(cfg, rep))
+
+
+def test_config0_all_seeds():
+    for rep in range(2, 5):
+        full_parity(make_config_chain(0, rep))
+
+
+def fuzz_chains():
+    out = []
+    rng = np.random.default_rng(12345)
+    for seed in range(24):
+        L = int(rng.integers(1, 41))
+        K = int(rng.integers(1, 17))
+        uniform = seed % 4 == 3
+        ch = make_random_chain(5000 + seed, L, K, allow_zero=seed % 3 == 0, uniform=uniform,
+                               small_times=seed % 2 == 0, xmax=int(rng.integers(1, 12)),
+                               amax=int(rng.integers(0, 20)), tmax=int(rng.integers(0, 8)), tmin=0)
+        hi = store_all_bound(ch)
+        # budgets from nothing to beyond keeping everything, with ragged widths
+        M = int(rng.choice([0, 1, hi // 3, hi // 2, hi, 2 * hi + 37, 255, 256, 257]))
+        out.append((ch, M))
+    return out
+
+
+@pytest.mark.parametrize("idx", range(24))
+def test_fuzz_full_tables(idx):
+    ch, M = fuzz_chains()[idx]
+    full_parity(ch, M)
+
+
+def test_single_block_and_tiny_budgets():
+    ch = make_random_chain(77, 1, 4)
+    for M in (0, 1, 5, 63, 64, 65, 200):
+        full_parity(ch, M)
+
+
+def test_budget_below_x0_is_infeasible():
+    ch = make_config_chain(0)
+    s = rk.Solver(ch)
+    try:
+        assert s.solve(int(ch.x[0]) - 1) == INF
+        with pytest.raises(rk.RKError) as e:
+            s.schedule()
+        assert e.value.code == rk.RK_E_INFEASIBLE
+    finally:
+        s.close()
+
+
+def test_resolve_same_chain_different_budgets():
+    ch = make_config_chain(1)
+    s = rk.Solver(ch)
+    try:
+        for M in (1000, 400, 1500, 120, 1000):
+            sol = oracle.solve(ch, M)
+            assert s.solve(M) == sol.answer
+            opt, arg = s.rows()
+            o_opt, o_arg = sol.rows()
+            assert np.array_equal(opt, o_opt) and np.array_equal(arg, o_arg)
+    finally:
+        s.close()
+
+
+def test_async_in_torch_workspace_on_torch_stream():
+    import torch
+    ch = make_config_chain(1)
+    sol = oracle.solve(ch)
+    s = rk.Solver(ch)
+    try:
+        nbytes = s.workspace_bytes(ch.M)
+        ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+        st = torch.cuda.Stream()
+        s.solve_async(ch.M, ws.data_ptr(), nbytes, st.cuda_stream)
+        assert s.result() == sol.answer
+        opt, arg = s.rows()
+        o_opt, o_arg = sol.rows()
+        assert np.array_equal(opt, o_opt) and np.array_equal(arg, o_arg)
+        check_same_schedule(s, sol, ch, ch.M)
+        with pytest.raises(rk.RKError) as e:
+            s.solve_async(ch.M, ws.data_ptr(), nbytes - 1, st.cuda_stream)
+        assert e.value.code == rk.RK_E_NOMEM
+    finally:
+        s.close()
+
+
+def sub_rows_parity(s, ch, s0, n):
+    """Rows (s0+a, s0+b) of the full GPU table against the oracle on blocks s0..s0+n-1:
+    a span only involves its own blocks, so its row equals the sub-chain's."""
+    sub = ch.sub(s0, s0 + n - 1)
+    say(f"  sub-chain parity {ch.name} blocks {s0}..{s0 + n - 1}")
+    sol = oracle.solve(sub, s.M)
+    for a in range(n):
+        for b in range(a, n):
+            g_opt, g_arg = s.row(s0 + a, s0 + b)
+            o_opt, o_arg = sol.opt_row(a, b), sol.arg_row(a, b).astype(np.int32)
+            assert np.array_equal(g_opt, o_opt), (s0 + a, s0 + b)
+            exp = np.where(o_arg < 0, -1, np.where(o_arg >= n, o_arg - n + ch.L, o_arg + s0))
+            assert np.array_equal(g_arg.astype(np.int32), exp), (s0 + a, s0 + b)
+
+
+@pytest.mark.parametrize("cfg", [3, 4])
+def test_large_configs_sampled_and_properties(cfg):
+    """Full-size solve; exact parity on sampled sub-chains; properties on the whole table."""
+    ch = make_config_chain(cfg)
+    say(f"  solving {ch.name}")
+    s = rk.Solver(ch)
+    try:
+        ans = s.solve()
+        assert ans != INF
+        for s0, n in ((0, 24), (ch.L // 2, 20), (ch.L - 24, 24)):
+            sub_rows_parity(s, ch, s0, n)
+        # schedule: replays legally in the oracle's simulator at exactly the optimum
+        ops, nfwd = s.schedule()
+        ok, tm, pk, bad = oracle.simulate(ch, ops)
+        assert ok, bad
+        assert tm == ans and pk <= ch.M
+        # infeasibility pattern and monotonicity on sampled rows
+        mf = oracle.min_feasible(ch)
+        cells = oracle.cell_index(ch.L)
+        rng = np.random.default_rng(cfg)
+        m = np.arange(ch.M + 1)
+        for _ in range(60):
+            a = int(rng.integers(0, ch.L))
+            b = int(rng.integers(a, ch.L))
+            row, _ = s.row(a, b, want_arg=False)
+            assert np.array_equal(row != INF, m >= mf[cells[a, b]]), (a, b)
+            r64 = row.astype(np.int64)
+            assert (r64[1:] <= r64[:-1]).all(), (a, b)
+        row, _ = s.row(0, ch.L - 1, want_arg=False)
+        lb = (ch.fwd.astype(np.int64) + ch.bwd).min(axis=1).sum()
+        assert (row[row != INF] >= lb).all()
+    finally:
+        s.close()
+
+
+def test_profiling_counts_launches():
+    ch = make_config_chain(1)
+    s = rk.Solver(ch)
+    try:
+        s.set_profiling(True)
+        s.solve()
+        stats = s.kernel_stats()
+        total = sum(n for n, _ in stats.values())
+        ms, launches = s.fill_ms()
+        assert total == launches and launches >= 1
+        assert sum(t for _, t in stats.values()) <= ms * 1.05 + 0.05
+    finally:
+        s.close()
