@@ -103,10 +103,11 @@ def main():
         ans, nops = step()
         fm, _ = s.fill_ms()
         fill_ms.append(fm)
-        for name, (n, ms) in s.kernel_stats().items():
-            a = kern.setdefault(name, [0, 0.0])
+        for name, (n, ms, work) in s.kernel_stats().items():
+            a = kern.setdefault(name, [0, 0.0, 0])
             a[0] += n
             a[1] += ms
+            a[2] += work
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
@@ -122,18 +123,21 @@ def main():
     s.schedule()
     sched_ms = (time.perf_counter() - t) * 1e3
 
-    dom = max(kern.items(), key=lambda kv: kv[1][1])
-    dname, (dn, dms) = dom
+    # dominant kernel: the one with the most device time; its algorithmic work is the
+    # relaxations it performs (2 int32 ops each: an add and a min)
+    dname, (dn, dms, dwork) = max(kern.items(), key=lambda kv: kv[1][1])
     per_launch_ms = dms / dn
-    relax_per_launch = relax * args.steps / dn if len(kern) == 1 else None
-    achieved_tops = OPS_PER_RELAX * relax * args.steps / (dms * 1e-3) / 1e12 if len(kern) == 1 else None
+    ops_per_launch = OPS_PER_RELAX * dwork / dn
+    achieved_tops = ops_per_launch / (per_launch_ms * 1e-3) / 1e12
     roofline = {
         "bound": "alu", "kernel": dname,
         "achieved": achieved_tops, "peak": VALU_PEAK_TOPS, "unit": "TOP/s",
-        "frac": (achieved_tops / VALU_PEAK_TOPS) if achieved_tops else None,
+        "frac": achieved_tops / VALU_PEAK_TOPS,
         "traffic": None,
         "launches_per_step": dn / args.steps, "avg_launch_ms": per_launch_ms,
-        "ops_per_launch": OPS_PER_RELAX * relax_per_launch if relax_per_launch else None,
+        "ops_per_launch": ops_per_launch,
+        "whole_fill_frac": OPS_PER_RELAX * relax / (statistics.median(fill_ms) * 1e-3) / 1e12
+                           / VALU_PEAK_TOPS,
     }
 
     cpu = None
@@ -153,7 +157,8 @@ def main():
         "schedule_ms": sched_ms,
         "fill_relax_per_s": relax / (statistics.median(fill_ms) * 1e-3),
         "roofline": roofline, "cpu_baseline": cpu,
-        "kernels": {k: {"launches_per_step": v[0] / args.steps, "ms_per_step": v[1] / args.steps}
+        "kernels": {k: {"launches_per_step": v[0] / args.steps, "ms_per_step": v[1] / args.steps,
+                        "relaxations_per_step": v[2] // args.steps}
                     for k, v in kern.items()},
     }
     s.close()

@@ -145,12 +145,15 @@ int rk_last_fill_ms(rk_chain *c, float *ms, int32_t *launches);
  * kernel the fill launches is bracketed by a pair of HIP events on the solve's
  * stream.  rk_fill_kernel_stats then reports, for kernel kind `kind`
  * (0 <= kind < *n_kinds), its name as a profiler shows it, the number of its
- * launches in the last solve and their summed device time in milliseconds.
- * Waits for the last solve.  RK_E_INVAL for a kind out of range.
+ * launches in the last solve, their summed device time in milliseconds and the
+ * number of candidate evaluations of the recurrence (relaxations, counting
+ * only valid (s,t,m,choice) combinations) those launches performed.  Any
+ * output pointer may be NULL.  Waits for the last solve; timings need
+ * profiling to have been on during it.  RK_E_INVAL for a kind out of range.
  */
 int rk_set_profiling(rk_chain *c, int32_t enable);
 int rk_fill_kernel_stats(rk_chain *c, int32_t kind, int32_t *n_kinds, const char **name,
-                         int32_t *launches, float *total_ms);
+                         int32_t *launches, float *total_ms, int64_t *relaxations);
 
 /* Short English description of an RK_* code. */
 const char *rk_strerror(int code);

@@ -21,11 +21,13 @@ struct rk_chain {
     void *d_chain = nullptr;  // x | xbar | c1 | need1 | P | need2
     DevChain dc{};
 
-    void *own_ws = nullptr;  // table owned by the chain (rk_solve)
+    int32_t max_x = 0;       // largest x_i over the split points i = 1..L-1
+
+    void *own_ws = nullptr;  // tables owned by the chain (rk_solve)
     size_t own_ws_bytes = 0;
-    int32_t *tab = nullptr;  // table of the last solve (own or caller's)
+    rk::Tables tb{};         // tables of the last solve (own or caller's)
     hipStream_t stream = nullptr;
-    int32_t M = -1, W = 0, stride = 0;
+    int32_t M = -1, W = 0;
     bool queued = false;
 
     hipEvent_t ev_fill0 = nullptr, ev_fill1 = nullptr;
@@ -65,12 +67,21 @@ struct DeviceScope {
     }
 };
 
-int table_bytes(int32_t L, int32_t M, size_t *bytes)
+// Geometry of the two tables for budget M: the left pad covers every shift x_i that can
+// still land on a budget column; a larger x_i makes its operand infinite everywhere.
+struct Geometry {
+    int32_t W, padl, stride;
+    int64_t rows;  // span rows + the infinity row
+};
+
+int geometry(const rk_chain *c, int32_t M, Geometry *g, size_t *bytes)
 {
     if (M < 0 || M > RK_MAX_M) return RK_E_INVAL;
-    const int64_t rows = rk::n_rows(L);
-    const int64_t stride = rk::row_stride(M + 1);
-    const int64_t elems = rows * stride;
+    g->W = M + 1;
+    g->padl = rk::round64(std::min<int64_t>(c->max_x, g->W));
+    g->stride = g->padl + rk::round64(g->W);
+    g->rows = rk::n_rows(c->L) + 1;
+    const int64_t elems = 2 * g->rows * (int64_t)g->stride;
     if (elems <= 0 || elems > (int64_t(1) << 40)) return RK_E_NOMEM;
     *bytes = (size_t)elems * sizeof(int32_t);
     return RK_OK;
@@ -111,17 +122,21 @@ int ensure_device(rk_chain *c)
 
 int32_t to_abi(int32_t v) { return v >= DINF ? RK_INF : v; }
 
-int fill(rk_chain *c, int32_t M, int32_t *tab, hipStream_t stream)
+int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t stream)
 {
     c->queued = false;
     c->M = M;
-    c->W = M + 1;
-    c->stride = rk::row_stride(c->W);
-    c->tab = tab;
+    c->W = g.W;
+    c->tb.W = g.W;
+    c->tb.padl = g.padl;
+    c->tb.stride = g.stride;
+    c->tb.inf_row = g.rows - 1;
+    c->tb.opt = tables;
+    c->tb.ap = tables + g.rows * (int64_t)g.stride;
     c->stream = stream;
     c->prof.reset(stream);
     HIPCHK(hipEventRecord(c->ev_fill0, stream));
-    HIPCHK(rk::launch_fill(c->dc, tab, c->W, c->stride, stream, &c->launches, &c->prof));
+    HIPCHK(rk::launch_fill(c->dc, c->tb, stream, &c->launches, &c->prof));
     HIPCHK(hipEventRecord(c->ev_fill1, stream));
     c->queued = true;
     return RK_OK;
@@ -133,8 +148,8 @@ int answer(rk_chain *c, int32_t *out)
     HIPCHK(hipEventSynchronize(c->ev_fill1));
     if (c->M < c->x[0]) { *out = RK_INF; return RK_OK; }
     int32_t v = 0;
-    const int64_t idx = rk::row_of(c->L, 0, c->L - 1) * c->stride + (c->M - c->x[0]);
-    HIPCHK(hipMemcpy(&v, c->tab + idx, sizeof(int32_t), hipMemcpyDeviceToHost));
+    const int64_t idx = rk::row_of(c->L, 0, c->L - 1) * c->tb.stride + c->tb.padl + (c->M - c->x[0]);
+    HIPCHK(hipMemcpy(&v, c->tb.opt + idx, sizeof(int32_t), hipMemcpyDeviceToHost));
     *out = to_abi(v);
     return RK_OK;
 }
@@ -210,6 +225,7 @@ int rk_chain_create(int32_t L, int32_t K, const int32_t *x, const int32_t *fn_ti
             c->need2[(size_t)s * L + i] = (int32_t)std::min(need, kSizeCap);
         }
     }
+    for (int32_t i = 1; i < L; ++i) c->max_x = std::max(c->max_x, x[i]);
     *out = c;
     return RK_OK;
 }
@@ -235,14 +251,16 @@ void rk_chain_destroy(rk_chain *c)
 int rk_workspace_bytes(const rk_chain *c, int32_t M, size_t *bytes)
 {
     if (!c || !bytes) return RK_E_INVAL;
-    return table_bytes(c->L, M, bytes);
+    Geometry g;
+    return geometry(c, M, &g, bytes);
 }
 
 int rk_solve_async(rk_chain *c, int32_t M, void *d_workspace, size_t ws_bytes, void *stream)
 {
     if (!c) return RK_E_INVAL;
     size_t need = 0;
-    int rc = table_bytes(c->L, M, &need);
+    Geometry g;
+    int rc = geometry(c, M, &g, &need);
     if (rc != RK_OK) return rc;
     DeviceScope ds(c);
     if (!ds.ok) return RK_E_DEVICE;
@@ -266,7 +284,7 @@ int rk_solve_async(rk_chain *c, int32_t M, void *d_workspace, size_t ws_bytes, v
         }
         tab = static_cast<int32_t *>(c->own_ws);
     }
-    return fill(c, M, tab, static_cast<hipStream_t>(stream));
+    return fill(c, M, g, tab, static_cast<hipStream_t>(stream));
 }
 
 int rk_solve(rk_chain *c, int32_t M, int32_t *opt_out)
@@ -306,8 +324,8 @@ int rk_extract_schedule(rk_chain *c, rk_op *ops, int64_t cap, int64_t *n_ops, in
         if (hipMalloc(&c->d_ops, max_ops * sizeof(rk_op)) != hipSuccess) return RK_E_NOMEM;
         c->d_ops_cap = max_ops;
     }
-    HIPCHK(rk::launch_backtrace(c->dc, c->tab, c->stride, c->M - c->x[0], c->d_ops, c->d_ops_cap,
-                                c->d_res, c->stream));
+    HIPCHK(rk::launch_backtrace(c->dc, c->tb, c->M - c->x[0], c->d_ops, c->d_ops_cap, c->d_res,
+                                c->stream));
     int64_t res[3] = {0, 0, 0};
     HIPCHK(hipMemcpyAsync(res, c->d_res, sizeof(res), hipMemcpyDeviceToHost, c->stream));
     HIPCHK(hipStreamSynchronize(c->stream));
@@ -326,9 +344,9 @@ int rk_read_row(rk_chain *c, int32_t s, int32_t t, int32_t *opt_row, int16_t *ar
     DeviceScope ds(c);
     if (!ds.ok) return RK_E_DEVICE;
     HIPCHK(hipEventSynchronize(c->ev_fill1));
-    const int64_t base = rk::row_of(c->L, s, t) * c->stride;
+    const int64_t base = rk::row_of(c->L, s, t) * c->tb.stride + c->tb.padl;
     if (opt_row) {
-        HIPCHK(hipMemcpy(opt_row, c->tab + base, (size_t)c->W * sizeof(int32_t), hipMemcpyDeviceToHost));
+        HIPCHK(hipMemcpy(opt_row, c->tb.opt + base, (size_t)c->W * sizeof(int32_t), hipMemcpyDeviceToHost));
         for (int32_t m = 0; m < c->W; ++m) opt_row[m] = to_abi(opt_row[m]);
     }
     if (arg_row) {
@@ -339,7 +357,7 @@ int rk_read_row(rk_chain *c, int32_t s, int32_t t, int32_t *opt_row, int16_t *ar
             if (hipMalloc(&c->d_argrow, (size_t)c->W * sizeof(int16_t)) != hipSuccess) return RK_E_NOMEM;
             c->d_argrow_cap = c->W;
         }
-        HIPCHK(rk::launch_arg_row(c->dc, c->tab, c->W, c->stride, s, t, c->d_argrow, c->stream));
+        HIPCHK(rk::launch_arg_row(c->dc, c->tb, s, t, c->d_argrow, c->stream));
         HIPCHK(hipMemcpyAsync(arg_row, c->d_argrow, (size_t)c->W * sizeof(int16_t),
                               hipMemcpyDeviceToHost, c->stream));
         HIPCHK(hipStreamSynchronize(c->stream));
@@ -367,7 +385,7 @@ int rk_set_profiling(rk_chain *c, int32_t enable)
 }
 
 int rk_fill_kernel_stats(rk_chain *c, int32_t kind, int32_t *n_kinds, const char **name,
-                         int32_t *launches, float *total_ms)
+                         int32_t *launches, float *total_ms, int64_t *relaxations)
 {
     if (!c) return RK_E_INVAL;
     if (n_kinds) *n_kinds = rk::KFILL_NKINDS;
@@ -388,6 +406,7 @@ int rk_fill_kernel_stats(rk_chain *c, int32_t kind, int32_t *n_kinds, const char
     }
     if (launches) *launches = cnt;
     if (total_ms) *total_ms = sum;
+    if (relaxations) *relaxations = c->prof.work[kind];
     return RK_OK;
 }
 

@@ -1,17 +1,24 @@
 // rk_internal.h -- shared definitions of librkrotor's host code and HIP kernels.
 //
-// Table layout in HBM (one row per span, diagonal-major):
+// Tables in HBM.  One row per span (s,t), diagonal-major:
 //   row(s,t) = off(d) + s with d = t - s and off(d) = sum_{d' < d} (L - d'),
-//   element (s,t,m) at tab[row(s,t) * stride + m], m in [0, W), W = M + 1,
-//   stride = W rounded up to a multiple of 64 int32 (256 B) so every row starts
-//   on a 256-byte boundary.
-// A span-length diagonal is thus a contiguous slab of (L - d) rows.
+// so a span-length diagonal is a contiguous slab of L - d rows; one more row
+// (index n_rows) holds only "infinity".  A row is `stride` int32 wide: `padl`
+// columns of infinity, then the W = M + 1 budget columns m = 0..M, then
+// padding to a multiple of 64 (256 B) so every row starts 256-byte aligned.
 //
-// Inside the device code "infinity" is DINF = 2^30 - 1: a saturated partial
-// sum (at most DINF) plus a table value (at most DINF) still fits in int32, so
-// the hot loops need no 64-bit or saturating arithmetic.  Every finite value
-// is at most RK_TIME_LIMIT < DINF (checked when the chain is created); the
-// host turns DINF into RK_INF on the way out.
+//   opt  Opt(s,t,m) at opt[row(s,t)*stride + padl + m].  The left pad lets a
+//        read at m - x_i (Eq. fn's right subproblem) run unmasked: columns
+//        below 0 read infinity.  Before a span is final its slot holds the
+//        partial minimum that the band products left there.
+//   ap   the left operand of Eq. fn, precomputed when a row becomes final:
+//        ap[row(s,i-1)*stride + padl + m] = P[s][i] + Opt(s,i-1,m) if the
+//        no-save sweep s..i-1 fits in m, else infinity (saturated).
+//
+// Inside the device code "infinity" is DINF = 2^30 - 1: ap (at most DINF) plus
+// an Opt value (at most DINF) fits in int32, so the hot loops are a plain add
+// and a min.  Every finite value is at most RK_TIME_LIMIT < DINF (checked
+// when the chain is created); the host turns DINF into RK_INF on the way out.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -26,6 +33,10 @@ namespace rk {
 constexpr int32_t DINF = (1 << 30) - 1;
 static_assert(RK_TIME_LIMIT < DINF, "finite values must stay below the device infinity");
 
+// Spans per band: every band of BAND span lengths gets one tiled product over
+// the splits whose two operands are older than the band.
+constexpr int32_t BAND = 16;
+
 // Per-chain arrays derived on the host (App. C quantities), resident on the device.
 struct DevChain {
     int32_t L, K;
@@ -37,6 +48,13 @@ struct DevChain {
     const int32_t *need2;  // [L*L]  smallest m at which the sweep s..i-1 is valid (i > s)
 };
 
+struct Tables {
+    int32_t *opt;
+    int32_t *ap;
+    int32_t W, stride, padl;
+    int64_t inf_row;  // index of the all-infinity row (= number of span rows)
+};
+
 __host__ __device__ inline int64_t row_of(int32_t L, int32_t s, int32_t t)
 {
     const int64_t d = t - s;
@@ -44,7 +62,7 @@ __host__ __device__ inline int64_t row_of(int32_t L, int32_t s, int32_t t)
 }
 
 inline int64_t n_rows(int32_t L) { return (int64_t)L * (L + 1) / 2; }
-inline int32_t row_stride(int32_t W) { return (W + 63) / 64 * 64; }
+inline int32_t round64(int64_t v) { return (int32_t)((v + 63) / 64 * 64); }
 
 // Optional per-launch event bracketing of the fill kernels (benchmark timing).
 struct Profiler {
@@ -53,24 +71,32 @@ struct Profiler {
     std::vector<hipEvent_t> events;  // pool, 2 per launch
     std::vector<int32_t> kinds;      // kernel kind of each bracketed launch
     int32_t n = 0;                   // launches bracketed in the current solve
+    int64_t work[8] = {};            // relaxations per kernel kind in the current solve
     hipError_t before(int32_t kind);
     hipError_t after();
-    void reset(hipStream_t s) { stream = s; n = 0; kinds.clear(); }
+    void reset(hipStream_t s)
+    {
+        stream = s;
+        n = 0;
+        kinds.clear();
+        for (int64_t &w : work) w = 0;
+    }
 };
 
 // Kernel kinds of the fill, in the order rk_fill_kernel_stats reports them.
-enum FillKernel : int32_t { KFILL_DIAG = 0, KFILL_NKINDS };
+enum FillKernel : int32_t { KFILL_PRODUCT = 0, KFILL_FINALIZE, KFILL_INIT, KFILL_NKINDS };
+static_assert(KFILL_NKINDS <= 8, "Profiler::work holds 8 kinds");
 extern const char *const kFillKernelNames[KFILL_NKINDS];
 
 // Launchers (rk_kernels.hip).  All return hipError_t of the launch.
-hipError_t launch_fill(const DevChain &ch, int32_t *tab, int32_t W, int32_t stride,
-                       hipStream_t stream, int32_t *launches, Profiler *prof);
-hipError_t launch_arg_row(const DevChain &ch, const int32_t *tab, int32_t W, int32_t stride,
-                          int32_t s, int32_t t, int16_t *out, hipStream_t stream);
+hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream, int32_t *launches,
+                       Profiler *prof);
+hipError_t launch_arg_row(const DevChain &ch, const Tables &tb, int32_t s, int32_t t, int16_t *out,
+                          hipStream_t stream);
 // Alg. 3 on the device; res[0] = number of steps, res[1] = index of the first
 // backward, res[2] = status (0 ok, 1 infeasible cell, 2 inconsistent table,
 // 3 stack overflow).
-hipError_t launch_backtrace(const DevChain &ch, const int32_t *tab, int32_t stride, int32_t m_top,
-                            rk_op *ops, int64_t cap, int64_t *res, hipStream_t stream);
+hipError_t launch_backtrace(const DevChain &ch, const Tables &tb, int32_t m_top, rk_op *ops,
+                            int64_t cap, int64_t *res, hipStream_t stream);
 
 }  // namespace rk

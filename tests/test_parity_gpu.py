@@ -13,7 +13,7 @@ import pytest
 import oracle
 from paper_2307_01236_amd import rk
 from paper_2307_01236_amd.chaingen import (CONFIGS, make_config_chain, make_random_chain,
-                                            store_all_bound)
+                                            relaxations, store_all_bound)
 
 pytestmark = pytest.mark.gpu
 INF = rk.RK_INF
@@ -204,9 +204,11 @@ def test_profiling_counts_launches():
         s.set_profiling(True)
         s.solve()
         stats = s.kernel_stats()
-        total = sum(n for n, _ in stats.values())
+        total = sum(v[0] for v in stats.values())
         ms, launches = s.fill_ms()
         assert total == launches and launches >= 1
-        assert sum(t for _, t in stats.values()) <= ms * 1.05 + 0.05
+        assert sum(v[1] for v in stats.values()) <= ms * 1.05 + 0.05
+        # the kernels' relaxation counts add up to the recurrence's candidate count
+        assert sum(v[2] for v in stats.values()) == relaxations(ch.L, ch.K, ch.M)
     finally:
         s.close()
