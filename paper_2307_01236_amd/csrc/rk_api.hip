@@ -15,7 +15,7 @@ using rk::DINF;
 
 struct rk_chain {
     int32_t L = 0, K = 0;
-    std::vector<int32_t> x, xbar, c1, need1, P, need2;  // host copies of the device arrays
+    std::vector<int32_t> x, xbar, c1, need1, need1max, P, need2;  // host copies of the device arrays
 
     int device = -1;
     void *d_chain = nullptr;  // x | xbar | c1 | need1 | P | need2
@@ -93,7 +93,7 @@ int ensure_device(rk_chain *c)
     if (c->d_chain) return RK_OK;
     const int32_t L = c->L, K = c->K;
     const size_t nx = L + 1, nk = (size_t)L * K, nl = (size_t)L * L;
-    const size_t total = nx + 3 * nk + 2 * nl;
+    const size_t total = nx + 3 * nk + L + 2 * nl;
     HIPCHK(hipMalloc(&c->d_chain, total * sizeof(int32_t)));
     int32_t *p = static_cast<int32_t *>(c->d_chain);
     size_t off = 0;
@@ -110,9 +110,11 @@ int ensure_device(rk_chain *c)
     c->dc.xbar = put(c->xbar);
     c->dc.c1 = put(c->c1);
     c->dc.need1 = put(c->need1);
+    c->dc.need1max = put(c->need1max);
     c->dc.P = put(c->P);
     c->dc.need2 = put(c->need2);
-    if (!c->dc.x || !c->dc.xbar || !c->dc.c1 || !c->dc.need1 || !c->dc.P || !c->dc.need2)
+    if (!c->dc.x || !c->dc.xbar || !c->dc.c1 || !c->dc.need1 || !c->dc.need1max || !c->dc.P ||
+        !c->dc.need2)
         return RK_E_DEVICE;
     HIPCHK(hipEventCreate(&c->ev_fill0));
     HIPCHK(hipEventCreate(&c->ev_fill1));
@@ -131,6 +133,7 @@ int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t
     c->tb.padl = g.padl;
     c->tb.stride = g.stride;
     c->tb.inf_row = g.rows - 1;
+    c->tb.max_x = c->max_x;
     c->tb.opt = tables;
     c->tb.ap = tables + g.rows * (int64_t)g.stride;
     c->stream = stream;
@@ -197,6 +200,7 @@ int rk_chain_create(int32_t L, int32_t K, const int32_t *x, const int32_t *fn_ti
         c->xbar.resize(nk);
         c->c1.resize(nk);
         c->need1.resize(nk);
+        c->need1max.assign(L, 0);
         c->P.assign((size_t)L * L, 0);
         c->need2.assign((size_t)L * L, 0);
     } catch (...) {
@@ -212,6 +216,7 @@ int rk_chain_create(int32_t L, int32_t K, const int32_t *x, const int32_t *fn_ti
             c->xbar[j] = (int32_t)std::min(xb, kSizeCap);
             c->need1[j] = (int32_t)std::min(xb + std::max(tmp_fwd[j], tmp_bwd[j]), kSizeCap);
             c->c1[j] = fwd[j] + bwd[j];
+            c->need1max[s] = std::max(c->need1max[s], c->need1[j]);
         }
     // Case 2 (Eq. fn): the sweep F_s^0..F_{i-1}^0 costs P[s][i]; F_k^0 holds its input
     // (except the span input x_s, outside the budget), its output and tmp(F_k^0).

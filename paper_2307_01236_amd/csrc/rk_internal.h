@@ -1,8 +1,9 @@
 // rk_internal.h -- shared definitions of librkrotor's host code and HIP kernels.
 //
-// Tables in HBM.  One row per span (s,t), diagonal-major:
-//   row(s,t) = off(d) + s with d = t - s and off(d) = sum_{d' < d} (L - d'),
-// so a span-length diagonal is a contiguous slab of L - d rows; one more row
+// Tables in HBM.  One row per span (s,t), row-major over the upper triangle:
+//   row(s,t) = s L - s (s-1)/2 + (t - s),
+// so the spans that start at s are consecutive rows (the right operands
+// Opt(i, t..t+n) of one split i are n+1 neighbouring rows); one more row
 // (index n_rows) holds only "infinity".  A row is `stride` int32 wide: `padl`
 // columns of infinity, then the W = M + 1 budget columns m = 0..M, then
 // padding to a multiple of 64 (256 B) so every row starts 256-byte aligned.
@@ -44,6 +45,7 @@ struct DevChain {
     const int32_t *xbar;   // [L*K]  x_{s+1} + mem_s^o: what F_s^o leaves live
     const int32_t *c1;     // [L*K]  r(F_s^o) + r(B_s^o)
     const int32_t *need1;  // [L*K]  smallest m at which option o of block s is valid
+    const int32_t *need1max;  // [L] max_o need1[s][o]: every option of block s is valid from here
     const int32_t *P;      // [L*L]  P[s*L+i] = sum_{k=s}^{i-1} r(F_k^0)        (i > s)
     const int32_t *need2;  // [L*L]  smallest m at which the sweep s..i-1 is valid (i > s)
 };
@@ -52,13 +54,13 @@ struct Tables {
     int32_t *opt;
     int32_t *ap;
     int32_t W, stride, padl;
+    int32_t max_x;    // largest x_i over the split points; > padl means some shifts leave the row
     int64_t inf_row;  // index of the all-infinity row (= number of span rows)
 };
 
 __host__ __device__ inline int64_t row_of(int32_t L, int32_t s, int32_t t)
 {
-    const int64_t d = t - s;
-    return d * L - d * (d - 1) / 2 + s;
+    return (int64_t)s * L - (int64_t)s * (s - 1) / 2 + (t - s);
 }
 
 inline int64_t n_rows(int32_t L) { return (int64_t)L * (L + 1) / 2; }

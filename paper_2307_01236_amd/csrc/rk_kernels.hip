@@ -51,30 +51,77 @@ __global__ __launch_bounds__(256) void k_init_inf_rows(Tables tb)
 }
 
 // ---------------------------------------------------------------------------------------
-// Band product.  For the spans d in [tau, tau + T) (one band), the part of Eq. fn over
-// the splits i whose two operands are older than the band: both s..i-1 and i..t shorter
-// than tau.  That is a min-plus product
-//     acc(s,t) = min_i ap(s,i) + Opt(i, t, m - x_i)
-// elementwise in m.  A wavefront owns 64 consecutive budgets (lane = m) and SR rows s;
-// each of its lanes keeps SR x T accumulators, so every loaded ap value is used T times
-// and every loaded Opt value up to SR times.  Operands outside the window (not final
-// yet, or not a span) are read from the infinity row, which keeps the loop free of masks.
-// The partial minimum goes into the Opt slot of each cell; the finalize kernel of its
-// diagonal completes it.
+// Raw buffer loads: a descriptor per operand block, a fixed per-lane byte offset per row.
+// Reads past the descriptor's range return 0 instead of faulting; every such read is
+// also one whose value the kernel replaces by infinity.
 // ---------------------------------------------------------------------------------------
-template <int T, int SR>
-__global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t tau)
+__device__ inline __amdgpu_buffer_rsrc_t block_rsrc(const int32_t *base, const int32_t *end)
 {
+    const int64_t bytes = (const char *)end - (const char *)base;
+    const uint32_t n = bytes > 0xffffffffll ? 0xffffffffu : (uint32_t)bytes;
+    return __builtin_amdgcn_make_buffer_rsrc((void *)base, (short)0, (int)n, 0x00020000);
+}
+
+__device__ inline int32_t block_load(__amdgpu_buffer_rsrc_t r, uint32_t byte_off)
+{
+    return __builtin_amdgcn_raw_buffer_load_b32(r, (int)byte_off, 0, 0);
+}
+
+// ---------------------------------------------------------------------------------------
+// Band product.  For the spans d in [tau, tau + T) (one band), the part of Eq. fn over
+// the splits i whose two operands are older than the band (both s..i-1 and i..t shorter
+// than tau).  That is a min-plus product, elementwise in m:
+//     acc(s,t) = min_i ap(s,i) + Opt(i, t, m - x_i).
+// A workgroup owns 64 consecutive budgets (lane = m) and SW = 16 consecutive rows s; its
+// wave w keeps, per lane, the SR x T accumulators of rows s0..s0+SR-1 (s0 = S0 + SR w)
+// and ends t = s + tau + k.  Splits are taken CI at a time.  The right operands
+// Opt(i, t, .) of a chunk, for all NQ ends of the workgroup, are staged in LDS (each
+// global row read once, then used by up to SR waves x rows); each wave reads its own left
+// operands ap(s, i).  The next chunk's operands are fetched into registers while the
+// current one is relaxed.  Operands that are not final yet or are not spans become
+// infinity; chunks where all operands are known valid skip those checks.
+// ---------------------------------------------------------------------------------------
+template <int T>
+__global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t tau, int32_t x_fit)
+{
+    constexpr int SR = 4, NW = 4, SW = SR * NW, CI = 4;
+    constexpr int NQ = (SW + T - 1 + NW - 1) / NW * NW;  // staged ends, padded to the waves
+    constexpr int JW = NQ / NW;                           // staged rows per wave and split
+    static_assert(CI % 2 == 0, "splits are relaxed in pairs");
+    __shared__ int32_t qs[CI * NQ * 64];
+
     const int32_t L = ch.L;
-    const int32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int32_t m = blockIdx.x * 64 + lane;
-    const int32_t s0 = (blockIdx.y * 4 + wave) * SR;
+    const uint32_t lane = threadIdx.x & 63;
+    // wave index as a scalar: every row choice below is wave-uniform
+    const int32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int32_t S0 = blockIdx.y * SW;
     const int32_t s_end = L - tau;  // rows that own at least one cell of the band
-    if (s0 >= s_end) return;
+    if (S0 >= s_end) return;        // the whole workgroup leaves together
+    const int32_t s0 = S0 + wave * SR;
     const int64_t stride = tb.stride;
-    const int32_t col = tb.padl + min(m, tb.W - 1);
-    const int32_t *const inf_a = tb.ap + tb.inf_row * stride + col;
-    const int32_t *const inf_q = tb.opt + tb.inf_row * stride + col;
+    const uint32_t m = blockIdx.x * 64 + lane;
+    const uint32_t colb = (uint32_t)(tb.padl + min(m, (uint32_t)tb.W - 1)) * 4u;
+    const uint32_t pitch = (uint32_t)stride * 4u;
+    const int32_t *const opt_end = tb.opt + (tb.inf_row + 1) * stride;
+    const int32_t *const ap_end = tb.ap + (tb.inf_row + 1) * stride;
+    const int32_t t0 = S0 + tau;  // first end the workgroup covers
+    const int32_t i_lo = S0 + 1, i_hi = min(S0 + SW - 1 + tau, L - 1);
+
+    // right operands: this wave stages ends t0 + wave + NW*jj, which for one split i are
+    // rows (i, t0) + wave + NW*jj (the spans starting at i are consecutive rows)
+    uint32_t qoff[JW];
+#pragma unroll
+    for (int jj = 0; jj < JW; ++jj) qoff[jj] = (uint32_t)(jj * NW + wave) * pitch + colb;
+    // left operands: row (s0 + r, i - 1) is sum_{s'=s0}^{s0+r-1} (L - 1 - s') rows after (s0, i - 1)
+    uint32_t aoff[SR];
+    {
+        uint32_t delta = 0;
+#pragma unroll
+        for (int r = 0; r < SR; ++r) {
+            aoff[r] = delta * pitch + colb;
+            delta += (uint32_t)(L - 1 - (s0 + r));
+        }
+    }
 
     int32_t acc[SR][T];
 #pragma unroll
@@ -82,31 +129,71 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
 #pragma unroll
         for (int k = 0; k < T; ++k) acc[r][k] = DINF;
 
-    const int32_t i_lo = s0 + 1;
-    const int32_t i_hi = min(s0 + SR - 1 + tau, L - 1);
-    for (int32_t i = i_lo; i <= i_hi; ++i) {
-        int32_t a[SR];
+    int32_t qv[CI][JW], av[CI][SR];
+    auto fetch = [&](int32_t ic) {
+        const bool q_core = x_fit && ic + CI - 1 <= i_hi && ic + CI - 1 <= t0 &&
+                            t0 + NQ - 1 - ic < tau && t0 + NQ - 1 < L;
+        const bool a_core = s0 + SR - 1 < s_end && ic >= s0 + SR && ic + CI - 1 <= s0 + tau &&
+                            ic + CI - 1 <= i_hi;
 #pragma unroll
-        for (int r = 0; r < SR; ++r) {
-            const int32_t s = s0 + r, span = i - 1 - s;
-            const bool ok = s < s_end && span >= 0 && span < tau;
-            a[r] = ok ? tb.ap[row_of(L, s, i - 1) * stride + col] : *inf_a;
+        for (int ii = 0; ii < CI; ++ii) {
+            const int32_t i = ic + ii, ic_ = min(i, L - 1);
+            const int32_t xi = ch.x[ic_], xs = min(xi, tb.padl);
+            const int32_t *const qb = tb.opt + row_of(L, ic_, t0) * stride - xs;
+            const __amdgpu_buffer_rsrc_t rq = block_rsrc(qb, opt_end);
+#pragma unroll
+            for (int jj = 0; jj < JW; ++jj) {
+                const int32_t v = block_load(rq, qoff[jj]);
+                if (q_core) {
+                    qv[ii][jj] = v;
+                } else {
+                    const int32_t t = t0 + jj * NW + wave, span = t - i;
+                    const bool ok = (i <= i_hi) & (t < L) & (span >= 0) & (span < tau) &
+                                    (xi <= tb.padl);
+                    qv[ii][jj] = ok ? v : DINF;
+                }
+            }
+            const int32_t *const ab = tb.ap + row_of(L, s0, min(i, L) - 1) * stride;
+            const __amdgpu_buffer_rsrc_t ra = block_rsrc(ab, ap_end);
+#pragma unroll
+            for (int r = 0; r < SR; ++r) {
+                const int32_t v = block_load(ra, aoff[r]);
+                if (a_core) {
+                    av[ii][r] = v;
+                } else {
+                    const int32_t s = s0 + r, span = i - 1 - s;
+                    const bool ok = (i <= i_hi) & (s < s_end) & (span >= 0) & (span < tau);
+                    av[ii][r] = ok ? v : DINF;
+                }
+            }
         }
-        const int32_t xi = ch.x[i];
-        const bool xok = xi <= tb.padl;
-        int32_t q[SR + T - 1];
+    };
+
+    const int32_t *const qw = qs + wave * SR * 64 + lane;
+    fetch(i_lo);
+    for (int32_t ic = i_lo; ic <= i_hi; ic += CI) {
+        int32_t a[CI][SR];
 #pragma unroll
-        for (int j = 0; j < SR + T - 1; ++j) {
-            const int32_t t = s0 + tau + j, span = t - i;
-            const bool ok = xok && t < L && span >= 0 && span < tau;
-            q[j] = ok ? tb.opt[row_of(L, i, t) * stride + (col - xi)] : *inf_q;
+        for (int ii = 0; ii < CI; ++ii) {
+#pragma unroll
+            for (int jj = 0; jj < JW; ++jj) qs[(ii * NQ + jj * NW + wave) * 64 + lane] = qv[ii][jj];
+#pragma unroll
+            for (int r = 0; r < SR; ++r) a[ii][r] = av[ii][r];
         }
+        __syncthreads();
+        if (ic + CI <= i_hi) fetch(ic + CI);  // in flight while this chunk is relaxed
+        // acc(s0+r, s0+r+tau+k) = min(acc, ap(s0+r, i) + Opt(i, s0+r+tau+k, m - x_i)), two splits per min
 #pragma unroll
-        for (int r = 0; r < SR; ++r)
+        for (int ii = 0; ii < CI; ii += 2)
 #pragma unroll
-            for (int k = 0; k < T; ++k) acc[r][k] = min(acc[r][k], a[r] + q[r + k]);
+            for (int r = 0; r < SR; ++r)
+#pragma unroll
+                for (int k = 0; k < T; ++k)
+                    acc[r][k] = min(acc[r][k], min(a[ii][r] + qw[(ii * NQ + r + k) * 64],
+                                                   a[ii + 1][r] + qw[((ii + 1) * NQ + r + k) * 64]));
+        __syncthreads();
     }
-    if (m >= tb.W) return;
+    if (m >= (uint32_t)tb.W) return;
 #pragma unroll
     for (int r = 0; r < SR; ++r)
 #pragma unroll
@@ -121,51 +208,97 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
 // partial minimum the splits it did not cover (one operand inside the current band:
 // max(i-1-s, t-i) >= D, D the band start) and case 1 (Eq. fe), clamps, writes Opt and
 // the row's left operand ap(s, t+1) for the spans that will split after t.
+// Row pointers advance incrementally (the ap rows of row s are consecutive; the right
+// operand row (i+1, t) is L-i-1 rows after (i, t)) and splits go four at a time so their
+// loads overlap.  A wave whose smallest budget already satisfies every option's memory
+// requirement runs case 1 without per-lane masks.
 // ---------------------------------------------------------------------------------------
+__device__ inline int32_t row_load(const int32_t *row, uint32_t byte_off)
+{
+    return *(const int32_t *)((const char *)row + byte_off);
+}
+
 __global__ __launch_bounds__(256) void k_finalize(DevChain ch, Tables tb, int32_t d)
 {
-    const int32_t s = blockIdx.y, L = ch.L, K = ch.K, t = s + d;
+    const int32_t L = ch.L, K = ch.K;
+    const int32_t s = blockIdx.y, t = s + d;
     const int32_t m = blockIdx.x * 256 + threadIdx.x;
+    const int32_t m0 = __builtin_amdgcn_readfirstlane((int32_t)(blockIdx.x * 256 + (threadIdx.x & ~63u)));
     const int64_t stride = tb.stride;
-    const int64_t row = row_of(L, s, t) * stride;
-    if (m < tb.padl) tb.opt[row + m] = DINF;  // keep the left pad infinite
+    const int32_t padl = tb.padl;
+    int32_t *const orow = tb.opt + row_of(L, s, t) * stride;
+    if (m < padl) orow[m] = DINF;  // keep the left pad infinite
     if (m >= tb.W) return;
-    const int32_t col = tb.padl + m;
+    const uint32_t colb = (uint32_t)(padl + m) * 4u;
     const int32_t D = (d / BAND) * BAND;
-    int32_t best = D > 0 ? tb.opt[row + col] : DINF;
+    int32_t best = D > 0 ? row_load(orow, colb) : DINF;
 
-    auto split = [&](int32_t i) {
-        const int32_t a = tb.ap[row_of(L, s, i - 1) * stride + col];
-        const int32_t xi = ch.x[i];
-        const int32_t q = xi <= tb.padl ? tb.opt[row_of(L, i, t) * stride + (col - xi)] : DINF;
-        best = min(best, a + q);
+    // splits i in [lo, hi]: ap(s, i) + Opt(i, t, m - x_i)
+    const int32_t *const aps = tb.ap + row_of(L, s, s) * stride;  // split s+1; split i is i-1-s rows on
+    auto splits = [&](int32_t lo, int32_t hi) {
+        if (lo > hi) return;
+        const int32_t *q = tb.opt + row_of(L, lo, t) * stride;  // row (i, t)
+        int32_t i = lo;
+        auto one = [&](int32_t ii, const int32_t *qr) {
+            const int32_t xi = ch.x[ii];
+            const int32_t a = row_load(aps + (int64_t)(ii - 1 - s) * stride, colb);
+            const int32_t v = row_load(qr - min(xi, padl), colb);
+            return a + (xi <= padl ? v : DINF);
+        };
+        for (; i + 3 <= hi; i += 4) {
+            const int32_t *q1 = q + (int64_t)(L - i - 1) * stride;
+            const int32_t *q2 = q1 + (int64_t)(L - i - 2) * stride;
+            const int32_t *q3 = q2 + (int64_t)(L - i - 3) * stride;
+            const int32_t v0 = one(i, q), v1 = one(i + 1, q1), v2 = one(i + 2, q2), v3 = one(i + 3, q3);
+            best = min(best, min(min(v0, v1), min(v2, v3)));
+            q = q3 + (int64_t)(L - i - 4) * stride;
+        }
+        for (; i <= hi; ++i) {
+            best = min(best, one(i, q));
+            q += (int64_t)(L - i - 1) * stride;
+        }
     };
     if (D == 0) {
-        for (int32_t i = s + 1; i <= t; ++i) split(i);
+        splits(s + 1, t);
     } else {
-        for (int32_t i = s + 1; i <= t - D; ++i) split(i);      // t - i >= D
-        for (int32_t i = s + D + 1; i <= t; ++i) split(i);      // i - 1 - s >= D
+        splits(s + 1, t - D);      // t - i >= D
+        splits(s + D + 1, t);      // i - 1 - s >= D
     }
+
     // case 1, option o: r(F_s^o) + r(B_s^o) + Opt(s+1,t,m-xbar), valid iff m >= need1[s][o]
-    const int64_t rest_row = d > 0 ? row_of(L, s + 1, t) * stride + tb.padl : 0;
-    for (int32_t o = 0; o < K; ++o) {
-        if (m >= ch.need1[s * K + o]) {
-            const int32_t rest = d > 0 ? tb.opt[rest_row + (m - ch.xbar[s * K + o])] : 0;
-            best = min(best, ch.c1[s * K + o] + rest);
+    const int32_t *const c1 = ch.c1 + s * K, *const need1 = ch.need1 + s * K, *const xbar = ch.xbar + s * K;
+    if (d == 0) {
+        for (int32_t o = 0; o < K; ++o)
+            if (m >= need1[o]) best = min(best, c1[o]);
+    } else {
+        const int32_t *const rest = tb.opt + row_of(L, s + 1, t) * stride;
+        if (m0 >= ch.need1max[s]) {
+            int32_t o = 0;
+            for (; o + 3 < K; o += 4) {
+                const int32_t v0 = c1[o] + row_load(rest - xbar[o], colb);
+                const int32_t v1 = c1[o + 1] + row_load(rest - xbar[o + 1], colb);
+                const int32_t v2 = c1[o + 2] + row_load(rest - xbar[o + 2], colb);
+                const int32_t v3 = c1[o + 3] + row_load(rest - xbar[o + 3], colb);
+                best = min(best, min(min(v0, v1), min(v2, v3)));
+            }
+            for (; o < K; ++o) best = min(best, c1[o] + row_load(rest - xbar[o], colb));
+        } else {
+            for (int32_t o = 0; o < K; ++o)
+                if (m >= need1[o]) best = min(best, c1[o] + row_load(rest - xbar[o], colb));
         }
     }
     best = min(best, DINF);
-    tb.opt[row + col] = best;
+    orow[padl + m] = best;
     if (t + 1 < L) {
         const int32_t i = t + 1;
-        tb.ap[row + col] = m >= ch.need2[s * L + i] ? min(ch.P[s * L + i] + best, DINF) : DINF;
+        tb.ap[row_of(L, s, t) * stride + padl + m] =
+            m >= ch.need2[s * L + i] ? min(ch.P[s * L + i] + best, DINF) : DINF;
     }
 }
 
 hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream, int32_t *launches,
                        Profiler *prof)
 {
-    constexpr int SR = 4;
     hipError_t e;
     int32_t n = 0;
     if ((e = prof->before(KFILL_INIT)) != hipSuccess) return e;
@@ -176,9 +309,10 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
     const int32_t fin_x = (max(tb.W, tb.padl) + 255) / 256;
     for (int32_t d = 0; d < ch.L; ++d) {
         if (d > 0 && d % BAND == 0) {
-            const dim3 grid((tb.W + 63) / 64, (ch.L - d + 4 * SR - 1) / (4 * SR));
+            const dim3 grid((tb.W + 63) / 64, (ch.L - d + 15) / 16);
             if ((e = prof->before(KFILL_PRODUCT)) != hipSuccess) return e;
-            hipLaunchKernelGGL((k_product<BAND, SR>), grid, dim3(256), 0, stream, ch, tb, d);
+            hipLaunchKernelGGL((k_product<BAND>), grid, dim3(256), 0, stream, ch, tb, d,
+                               (int32_t)(tb.max_x <= tb.padl));
             if ((e = hipGetLastError()) != hipSuccess) return e;
             if ((e = prof->after()) != hipSuccess) return e;
             ++n;
