@@ -129,12 +129,19 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
 #pragma unroll
         for (int k = 0; k < T; ++k) acc[r][k] = DINF;
 
+    // fetch(ic) only issues the loads of chunk ic and records, as wave-uniform bit masks,
+    // which of them are valid operands; the values are masked when they are first used
+    // (one chunk later), so the loads stay in flight while the current chunk is relaxed
+    static_assert(CI * JW <= 32 && CI * SR <= 32, "validity masks are 32-bit");
     int32_t qv[CI][JW], av[CI][SR];
+    uint32_t qmask = 0, amask = 0;
     auto fetch = [&](int32_t ic) {
         const bool q_core = x_fit && ic + CI - 1 <= i_hi && ic + CI - 1 <= t0 &&
                             t0 + NQ - 1 - ic < tau && t0 + NQ - 1 < L;
         const bool a_core = s0 + SR - 1 < s_end && ic >= s0 + SR && ic + CI - 1 <= s0 + tau &&
                             ic + CI - 1 <= i_hi;
+        qmask = 0;
+        amask = 0;
 #pragma unroll
         for (int ii = 0; ii < CI; ++ii) {
             const int32_t i = ic + ii, ic_ = min(i, L - 1);
@@ -143,43 +150,49 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
             const __amdgpu_buffer_rsrc_t rq = block_rsrc(qb, opt_end);
 #pragma unroll
             for (int jj = 0; jj < JW; ++jj) {
-                const int32_t v = block_load(rq, qoff[jj]);
-                if (q_core) {
-                    qv[ii][jj] = v;
-                } else {
-                    const int32_t t = t0 + jj * NW + wave, span = t - i;
-                    const bool ok = (i <= i_hi) & (t < L) & (span >= 0) & (span < tau) &
-                                    (xi <= tb.padl);
-                    qv[ii][jj] = ok ? v : DINF;
-                }
+                qv[ii][jj] = block_load(rq, qoff[jj]);
+                const int32_t t = t0 + jj * NW + wave, span = t - i;
+                const bool ok = q_core || ((i <= i_hi) & (t < L) & (span >= 0) & (span < tau) &
+                                           (xi <= tb.padl));
+                qmask |= (uint32_t)ok << (ii * JW + jj);
             }
             const int32_t *const ab = tb.ap + row_of(L, s0, min(i, L) - 1) * stride;
             const __amdgpu_buffer_rsrc_t ra = block_rsrc(ab, ap_end);
 #pragma unroll
             for (int r = 0; r < SR; ++r) {
-                const int32_t v = block_load(ra, aoff[r]);
-                if (a_core) {
-                    av[ii][r] = v;
-                } else {
-                    const int32_t s = s0 + r, span = i - 1 - s;
-                    const bool ok = (i <= i_hi) & (s < s_end) & (span >= 0) & (span < tau);
-                    av[ii][r] = ok ? v : DINF;
-                }
+                av[ii][r] = block_load(ra, aoff[r]);
+                const int32_t s = s0 + r, span = i - 1 - s;
+                const bool ok = a_core || ((i <= i_hi) & (s < s_end) & (span >= 0) & (span < tau));
+                amask |= (uint32_t)ok << (ii * SR + r);
             }
         }
     };
+    constexpr uint32_t QALL = CI * JW == 32 ? 0xffffffffu : (1u << (CI * JW)) - 1u;
+    constexpr uint32_t AALL = CI * SR == 32 ? 0xffffffffu : (1u << (CI * SR)) - 1u;
 
     const int32_t *const qw = qs + wave * SR * 64 + lane;
     fetch(i_lo);
     for (int32_t ic = i_lo; ic <= i_hi; ic += CI) {
         int32_t a[CI][SR];
+        const uint32_t qm = __builtin_amdgcn_readfirstlane(qmask), am = __builtin_amdgcn_readfirstlane(amask);
+        if (qm == QALL) {
 #pragma unroll
-        for (int ii = 0; ii < CI; ++ii) {
+            for (int ii = 0; ii < CI; ++ii)
 #pragma unroll
-            for (int jj = 0; jj < JW; ++jj) qs[(ii * NQ + jj * NW + wave) * 64 + lane] = qv[ii][jj];
+                for (int jj = 0; jj < JW; ++jj) qs[(ii * NQ + jj * NW + wave) * 64 + lane] = qv[ii][jj];
+        } else {
 #pragma unroll
-            for (int r = 0; r < SR; ++r) a[ii][r] = av[ii][r];
+            for (int ii = 0; ii < CI; ++ii)
+#pragma unroll
+                for (int jj = 0; jj < JW; ++jj)
+                    qs[(ii * NQ + jj * NW + wave) * 64 + lane] =
+                        (qm >> (ii * JW + jj)) & 1u ? qv[ii][jj] : DINF;
         }
+#pragma unroll
+        for (int ii = 0; ii < CI; ++ii)
+#pragma unroll
+            for (int r = 0; r < SR; ++r)
+                a[ii][r] = (am == AALL || ((am >> (ii * SR + r)) & 1u)) ? av[ii][r] : DINF;
         __syncthreads();
         if (ic + CI <= i_hi) fetch(ic + CI);  // in flight while this chunk is relaxed
         // acc(s0+r, s0+r+tau+k) = min(acc, ap(s0+r, i) + Opt(i, s0+r+tau+k, m - x_i)), two splits per min
