@@ -39,6 +39,23 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def measured_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter summary,
+    if it was taken on the kernel source as it is now; else (None, None)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None, None
+    with open(path) as f:
+        prof = json.load(f)
+    with open(os.path.join(ROOT, prof["kernels_source"]), "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()
+    k = prof["kernels"].get(kernel)
+    if sha != prof["kernels_source_sha256"] or k is None:
+        return None, None
+    return k["hbm_bytes_per_dispatch"], None
+
+
 def cpu_baseline(ch, nblocks: int):
     import oracle
     from paper_2307_01236_amd.chaingen import relaxations
@@ -62,7 +79,19 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=WORKLOAD_CFG)
     ap.add_argument("--cpu-blocks", type=int, default=96, help="oracle sample size (0: skip)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only copy a MIB-sized buffer 3 times (to scale HBM byte counters) and exit")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        import torch
+        n = args.calibrate_copy << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n, "copies": 3}), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the solver runs on a single MI355X and this build "
               f"has no multi-GPU path (asked for --gpus {args.gpus}).", file=sys.stderr)
@@ -129,11 +158,14 @@ def main():
     per_launch_ms = dms / dn
     ops_per_launch = OPS_PER_RELAX * dwork / dn
     achieved_tops = ops_per_launch / (per_launch_ms * 1e-3) / 1e12
+    traffic, hbm_frac = measured_traffic(ch.name, dname)
+    if traffic is not None:
+        hbm_frac = traffic / (per_launch_ms * 1e-3) / (HBM_PEAK_GBS * 1e9)
     roofline = {
         "bound": "alu", "kernel": dname,
         "achieved": achieved_tops, "peak": VALU_PEAK_TOPS, "unit": "TOP/s",
         "frac": achieved_tops / VALU_PEAK_TOPS,
-        "traffic": None,
+        "traffic": traffic, "traffic_hbm_frac": hbm_frac,
         "launches_per_step": dn / args.steps, "avg_launch_ms": per_launch_ms,
         "ops_per_launch": ops_per_launch,
         "whole_fill_frac": OPS_PER_RELAX * relax / (statistics.median(fill_ms) * 1e-3) / 1e12

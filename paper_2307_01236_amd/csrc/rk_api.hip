@@ -83,6 +83,9 @@ int geometry(const rk_chain *c, int32_t M, Geometry *g, size_t *bytes)
     g->rows = rk::n_rows(c->L) + 1;
     const int64_t elems = 2 * g->rows * (int64_t)g->stride;
     if (elems <= 0 || elems > (int64_t(1) << 40)) return RK_E_NOMEM;
+    // the band product addresses its operand rows with 32-bit byte offsets spanning up to
+    // 3L + 32 rows from a block base
+    if ((3 * (int64_t)c->L + 32) * g->stride * 4 >= (int64_t(1) << 32)) return RK_E_NOMEM;
     *bytes = (size_t)elems * sizeof(int32_t);
     return RK_OK;
 }
