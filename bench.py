@@ -113,7 +113,6 @@ def main():
     nbytes = s.workspace_bytes(M)
     ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
     stream = torch.cuda.Stream()
-    s.set_profiling(True)
 
     def step():
         s.solve_async(M, ws.data_ptr(), nbytes, stream.cuda_stream)
@@ -125,22 +124,31 @@ def main():
         ans, nops = step()
         log(f"warmup {i}: answer={ans} ops={nops}")
 
-    fill_ms, kern = [], {}
+    # timed steps: the production path (the fill replays its captured launch sequence);
+    # HIP events around each fill on the solve's stream give the device fill time
+    fill_ms = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
         ans, nops = step()
-        fm, _ = s.fill_ms()
-        fill_ms.append(fm)
+        fill_ms.append(s.fill_ms()[0])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, fill median {statistics.median(fill_ms):.3f} ms")
+
+    # the same steps again with every kernel launch bracketed by HIP events on the solve's
+    # stream (launched one by one): per-kernel durations for the roofline
+    s.set_profiling(True)
+    kern = {}
+    for i in range(args.steps):
+        step()
         for name, (n, ms, work) in s.kernel_stats().items():
             a = kern.setdefault(name, [0, 0.0, 0])
             a[0] += n
             a[1] += ms
             a[2] += work
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
-    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, fill median {statistics.median(fill_ms):.3f} ms")
+    s.set_profiling(False)
 
     # solve wall time without the schedule, warm (synchronous rk_solve on the library's table)
     wall = []

@@ -98,7 +98,7 @@ int rk_workspace_bytes(const rk_chain *c, int32_t M, size_t *bytes);
  * Fill Opt(s,t,m) for every span and every m in [0, M] (Alg. 2) in a table
  * the chain allocates (and reuses across solves), then return the answer
  * Opt(0, L-1, M - x_0) in *opt_out, or RK_INF when the budget admits no
- * schedule (including M < x_0).  Synchronous; runs on the null stream.
+ * schedule (including M < x_0).  Synchronous; runs on a stream the chain owns.
  * RK_E_NOMEM if the table cannot be allocated, RK_E_DEVICE on a HIP error.
  */
 int rk_solve(rk_chain *c, int32_t M, int32_t *opt_out);
@@ -106,8 +106,11 @@ int rk_solve(rk_chain *c, int32_t M, int32_t *opt_out);
 /*
  * Same fill, asynchronous, in caller memory: d_workspace is device memory of
  * at least rk_workspace_bytes(c, M) bytes (for instance a torch tensor) and
- * stream a hipStream_t (NULL: the null stream).  Returns once the work is
- * queued.  The workspace must stay allocated and untouched until the chain is
+ * stream a hipStream_t (NULL: a stream the chain owns).  Returns once the work
+ * is queued.  The fill's kernel sequence is captured into a HIP graph on first
+ * use and replayed while M, the workspace, the stream and the profiling switch
+ * stay the same; on a stream the caller is itself capturing, the kernels are
+ * launched directly (and become part of the caller's graph).  The workspace must stay allocated and untouched until the chain is
  * destroyed or solved again; the chain reads results from it.  Call
  * rk_result to wait and read the answer.
  */
@@ -145,7 +148,8 @@ int rk_last_fill_ms(rk_chain *c, float *ms, int32_t *launches);
 /*
  * Kernel-level timing (for benchmarks; off by default).  While enabled, every
  * kernel the fill launches is bracketed by a pair of HIP events on the solve's
- * stream.  rk_fill_kernel_stats then reports, for kernel kind `kind`
+ * stream, and the fill launches its kernels one by one instead of replaying a
+ * graph.  rk_fill_kernel_stats then reports, for kernel kind `kind`
  * (0 <= kind < *n_kinds), its name as a profiler shows it, the number of its
  * launches in the last solve, their summed device time in milliseconds and the
  * number of candidate evaluations of the recurrence (relaxations, counting

@@ -34,6 +34,15 @@ struct rk_chain {
     int32_t launches = 0;
     rk::Profiler prof;
 
+    // The fill's launch sequence is captured once into a HIP graph and replayed while the
+    // budget, the tables, the stream and the profiling switch stay the same.
+    hipStream_t own_stream = nullptr;  // used when the caller passes no stream
+    hipGraphExec_t gexec = nullptr;
+    int32_t g_M = -1;
+    const int32_t *g_tables = nullptr;
+    hipStream_t g_stream = nullptr;
+    bool g_prof = false;
+
     rk_op *d_ops = nullptr;  // backtrace output
     int64_t d_ops_cap = 0;
     int64_t *d_res = nullptr;
@@ -121,6 +130,7 @@ int ensure_device(rk_chain *c)
         return RK_E_DEVICE;
     HIPCHK(hipEventCreate(&c->ev_fill0));
     HIPCHK(hipEventCreate(&c->ev_fill1));
+    HIPCHK(hipStreamCreateWithFlags(&c->own_stream, hipStreamNonBlocking));
     HIPCHK(hipMalloc(&c->d_res, 4 * sizeof(int64_t)));
     return RK_OK;
 }
@@ -140,9 +150,45 @@ int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t
     c->tb.opt = tables;
     c->tb.ap = tables + g.rows * (int64_t)g.stride;
     c->stream = stream;
-    c->prof.reset(stream);
     HIPCHK(hipEventRecord(c->ev_fill0, stream));
-    HIPCHK(rk::launch_fill(c->dc, c->tb, stream, &c->launches, &c->prof));
+    const bool replay = c->gexec && c->g_M == M && c->g_tables == tables && c->g_stream == stream &&
+                        c->g_prof == c->prof.on;
+    if (replay) {
+        HIPCHK(hipGraphLaunch(c->gexec, stream));
+    } else {
+        if (c->gexec) (void)hipGraphExecDestroy(c->gexec);
+        c->gexec = nullptr;
+        c->prof.reset(stream);
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        bool captured = false;
+        // per-launch profiling events must be recorded on the stream itself (elapsed times
+        // of events recorded inside a graph are not available), so profiled fills launch
+        // directly
+        if (!c->prof.on && hipStreamIsCapturing(stream, &cs) == hipSuccess &&
+            cs == hipStreamCaptureStatusNone &&
+            hipStreamBeginCapture(stream, hipStreamCaptureModeThreadLocal) == hipSuccess) {
+            const hipError_t le = rk::launch_fill(c->dc, c->tb, stream, &c->launches, &c->prof);
+            hipGraph_t graph = nullptr;
+            const hipError_t ce = hipStreamEndCapture(stream, &graph);
+            if (le == hipSuccess && ce == hipSuccess && graph &&
+                hipGraphInstantiate(&c->gexec, graph, nullptr, nullptr, 0) == hipSuccess) {
+                captured = true;
+                c->g_M = M;
+                c->g_tables = tables;
+                c->g_stream = stream;
+                c->g_prof = c->prof.on;
+            }
+            if (graph) (void)hipGraphDestroy(graph);
+            (void)hipGetLastError();
+        }
+        if (captured) {
+            HIPCHK(hipGraphLaunch(c->gexec, stream));
+        } else {  // the stream is being captured by the caller, or capture is unavailable
+            c->gexec = nullptr;
+            c->prof.reset(stream);
+            HIPCHK(rk::launch_fill(c->dc, c->tb, stream, &c->launches, &c->prof));
+        }
+    }
     HIPCHK(hipEventRecord(c->ev_fill1, stream));
     c->queued = true;
     return RK_OK;
@@ -249,8 +295,10 @@ void rk_chain_destroy(rk_chain *c)
         if (c->d_ops) (void)hipFree(c->d_ops);
         if (c->d_res) (void)hipFree(c->d_res);
         if (c->d_argrow) (void)hipFree(c->d_argrow);
+        if (c->gexec) (void)hipGraphExecDestroy(c->gexec);
         if (c->ev_fill0) (void)hipEventDestroy(c->ev_fill0);
         if (c->ev_fill1) (void)hipEventDestroy(c->ev_fill1);
+        if (c->own_stream) (void)hipStreamDestroy(c->own_stream);
         for (hipEvent_t e : c->prof.events) (void)hipEventDestroy(e);
     }
     delete c;
@@ -292,7 +340,7 @@ int rk_solve_async(rk_chain *c, int32_t M, void *d_workspace, size_t ws_bytes, v
         }
         tab = static_cast<int32_t *>(c->own_ws);
     }
-    return fill(c, M, g, tab, static_cast<hipStream_t>(stream));
+    return fill(c, M, g, tab, stream ? static_cast<hipStream_t>(stream) : c->own_stream);
 }
 
 int rk_solve(rk_chain *c, int32_t M, int32_t *opt_out)

@@ -68,6 +68,19 @@ __device__ inline int32_t block_load(__amdgpu_buffer_rsrc_t r, uint32_t byte_off
 }
 
 // ---------------------------------------------------------------------------------------
+// Workgroups of a launch go to the 8 XCDs round-robin (id g to XCD g mod 8), and each XCD
+// has its own L2.  Renumbering them so that every XCD gets one contiguous range of logical
+// tiles puts tiles that share operand rows into the same L2 at about the same time.
+// A bijection of [0, G); correctness does not depend on the dispatch order.
+// ---------------------------------------------------------------------------------------
+__device__ inline uint32_t xcd_tile(uint32_t g, uint32_t G)
+{
+    constexpr uint32_t NX = 8;
+    const uint32_t x = g % NX, j = g / NX, base = G / NX, rem = G % NX;
+    return (x < rem ? x * (base + 1) : rem * (base + 1) + (x - rem) * base) + j;
+}
+
+// ---------------------------------------------------------------------------------------
 // Band product.  For the spans d in [tau, tau + T) (one band), the part of Eq. fn over
 // the splits i whose two operands are older than the band (both s..i-1 and i..t shorter
 // than tau).  That is a min-plus product, elementwise in m:
@@ -94,12 +107,14 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
     const uint32_t lane = threadIdx.x & 63;
     // wave index as a scalar: every row choice below is wave-uniform
     const int32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int32_t S0 = blockIdx.y * SW;
     const int32_t s_end = L - tau;  // rows that own at least one cell of the band
-    if (S0 >= s_end) return;        // the whole workgroup leaves together
+    const uint32_t n_rb = (uint32_t)(s_end + SW - 1) / SW;
+    const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);  // row blocks of a column chunk adjacent
+    const int32_t S0 = (int32_t)(tile % n_rb) * SW;
+    const uint32_t mchunk = tile / n_rb;
     const int32_t s0 = S0 + wave * SR;
     const int64_t stride = tb.stride;
-    const uint32_t m = blockIdx.x * 64 + lane;
+    const uint32_t m = mchunk * 64 + lane;
     const uint32_t colb = (uint32_t)(tb.padl + min(m, (uint32_t)tb.W - 1)) * 4u;
     const uint32_t pitch = (uint32_t)stride * 4u;
     const int32_t *const opt_end = tb.opt + (tb.inf_row + 1) * stride;
@@ -234,9 +249,12 @@ __device__ inline int32_t row_load(const int32_t *row, uint32_t byte_off)
 __global__ __launch_bounds__(256) void k_finalize(DevChain ch, Tables tb, int32_t d)
 {
     const int32_t L = ch.L, K = ch.K;
-    const int32_t s = blockIdx.y, t = s + d;
-    const int32_t m = blockIdx.x * 256 + threadIdx.x;
-    const int32_t m0 = __builtin_amdgcn_readfirstlane((int32_t)(blockIdx.x * 256 + (threadIdx.x & ~63u)));
+    const uint32_t n_mc = (uint32_t)(max(tb.W, tb.padl) + 255) / 256;
+    const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);  // column chunks of a row adjacent
+    const int32_t s = (int32_t)(tile / n_mc), t = s + d;
+    const int32_t mbase = (int32_t)(tile % n_mc) * 256;
+    const int32_t m = mbase + (int32_t)threadIdx.x;
+    const int32_t m0 = __builtin_amdgcn_readfirstlane(mbase + (int32_t)(threadIdx.x & ~63u));
     const int64_t stride = tb.stride;
     const int32_t padl = tb.padl;
     int32_t *const orow = tb.opt + row_of(L, s, t) * stride;
@@ -322,7 +340,7 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
     const int32_t fin_x = (max(tb.W, tb.padl) + 255) / 256;
     for (int32_t d = 0; d < ch.L; ++d) {
         if (d > 0 && d % BAND == 0) {
-            const dim3 grid((tb.W + 63) / 64, (ch.L - d + 15) / 16);
+            const dim3 grid(((tb.W + 63) / 64) * ((ch.L - d + 15) / 16));
             if ((e = prof->before(KFILL_PRODUCT)) != hipSuccess) return e;
             hipLaunchKernelGGL((k_product<BAND>), grid, dim3(256), 0, stream, ch, tb, d,
                                (int32_t)(tb.max_x <= tb.padl));
@@ -334,7 +352,7 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
                 prof->work[KFILL_PRODUCT] += (int64_t)(ch.L - dd) * (2 * d - dd) * tb.W;
         }
         if ((e = prof->before(KFILL_FINALIZE)) != hipSuccess) return e;
-        hipLaunchKernelGGL(k_finalize, dim3(fin_x, ch.L - d), dim3(256), 0, stream, ch, tb, d);
+        hipLaunchKernelGGL(k_finalize, dim3(fin_x * (ch.L - d)), dim3(256), 0, stream, ch, tb, d);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if ((e = prof->after()) != hipSuccess) return e;
         ++n;

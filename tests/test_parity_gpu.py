@@ -212,3 +212,28 @@ def test_profiling_counts_launches():
         assert sum(v[2] for v in stats.values()) == relaxations(ch.L, ch.K, ch.M)
     finally:
         s.close()
+
+
+def test_graph_replays_match_oracle():
+    """Repeated solves at one budget replay the captured launch sequence; each replay, with
+    other solves and read-backs in between, must still match the oracle exactly."""
+    ch, other = make_config_chain(1), make_config_chain(0)
+    sol, osol = oracle.solve(ch), oracle.solve(other)
+    o_opt, o_arg = sol.rows()
+    exp_ops = oracle.schedule(sol)
+    s, t = rk.Solver(ch), rk.Solver(other)
+    try:
+        for rep in range(4):
+            say(f"  replay {rep}")
+            assert s.solve() == sol.answer
+            opt, arg = s.rows(want_arg=rep == 0)
+            assert np.array_equal(opt, o_opt)
+            if rep == 0:
+                assert np.array_equal(arg, o_arg)
+            ops, nfwd = s.schedule()
+            assert np.array_equal(ops, exp_ops[0]) and nfwd == exp_ops[1]
+            assert t.solve() == osol.answer
+            s.set_profiling(rep % 2 == 1)  # switching profiling re-captures the sequence
+    finally:
+        s.close()
+        t.close()
