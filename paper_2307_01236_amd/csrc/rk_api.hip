@@ -90,11 +90,11 @@ int geometry(const rk_chain *c, int32_t M, Geometry *g, size_t *bytes)
     g->padl = rk::round64(std::min<int64_t>(c->max_x, g->W));
     g->stride = g->padl + rk::round64(g->W);
     g->rows = rk::n_rows(c->L) + 1;
-    const int64_t elems = 2 * g->rows * (int64_t)g->stride;
+    const int64_t elems = 2 * rk::table_rows(c->L) * (int64_t)g->stride;
     if (elems <= 0 || elems > (int64_t(1) << 40)) return RK_E_NOMEM;
-    // the band product addresses its operand rows with 32-bit byte offsets spanning up to
-    // 3L + 32 rows from a block base
-    if ((3 * (int64_t)c->L + 32) * g->stride * 4 >= (int64_t(1) << 32)) return RK_E_NOMEM;
+    // the band product addresses the operand rows of one chunk of splits with 32-bit byte
+    // offsets from a chunk base
+    if ((rk::PROD_CI * (int64_t)c->L + 64) * g->stride * 4 >= (int64_t(1) << 32)) return RK_E_NOMEM;
     *bytes = (size_t)elems * sizeof(int32_t);
     return RK_OK;
 }
@@ -125,6 +125,9 @@ int ensure_device(rk_chain *c)
     c->dc.need1max = put(c->need1max);
     c->dc.P = put(c->P);
     c->dc.need2 = put(c->need2);
+    int64_t xbar_max = 0;
+    for (int32_t v : c->xbar) xbar_max = std::max<int64_t>(xbar_max, v);
+    c->dc.xbar_halo = xbar_max > rk::HMAX ? rk::HMAX + 1 : rk::round64(xbar_max);
     if (!c->dc.x || !c->dc.xbar || !c->dc.c1 || !c->dc.need1 || !c->dc.need1max || !c->dc.P ||
         !c->dc.need2)
         return RK_E_DEVICE;
@@ -146,9 +149,8 @@ int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t
     c->tb.padl = g.padl;
     c->tb.stride = g.stride;
     c->tb.inf_row = g.rows - 1;
-    c->tb.max_x = c->max_x;
-    c->tb.opt = tables;
-    c->tb.ap = tables + g.rows * (int64_t)g.stride;
+    c->tb.opt = tables + rk::SLACK * (int64_t)g.stride;
+    c->tb.ap = c->tb.opt + rk::table_rows(c->L) * (int64_t)g.stride;
     c->stream = stream;
     HIPCHK(hipEventRecord(c->ev_fill0, stream));
     const bool replay = c->gexec && c->g_M == M && c->g_tables == tables && c->g_stream == stream &&

@@ -4,9 +4,12 @@
 //   row(s,t) = s L - s (s-1)/2 + (t - s),
 // so the spans that start at s are consecutive rows (the right operands
 // Opt(i, t..t+n) of one split i are n+1 neighbouring rows); one more row
-// (index n_rows) holds only "infinity".  A row is `stride` int32 wide: `padl`
-// columns of infinity, then the W = M + 1 budget columns m = 0..M, then
-// padding to a multiple of 64 (256 B) so every row starts 256-byte aligned.
+// (index n_rows) holds only "infinity", and SLACK more rows before row 0 and
+// after the infinity row keep every operand address a kernel forms in bounds
+// (operands that do not exist are read there and then discarded).  A row is
+// `stride` int32 wide: `padl` columns of infinity, then the W = M + 1 budget
+// columns m = 0..M, then padding to a multiple of 64 (256 B) so every row
+// starts 256-byte aligned.
 //
 //   opt  Opt(s,t,m) at opt[row(s,t)*stride + padl + m].  The left pad lets a
 //        read at m - x_i (Eq. fn's right subproblem) run unmasked: columns
@@ -20,6 +23,9 @@
 // an Opt value (at most DINF) fits in int32, so the hot loops are a plain add
 // and a min.  Every finite value is at most RK_TIME_LIMIT < DINF (checked
 // when the chain is created); the host turns DINF into RK_INF on the way out.
+// The band product adds with unsigned saturation instead: a candidate that is
+// not a split of its cell has one operand forced to DINF, and its other operand
+// may be any 32-bit pattern (a row not written yet), so the sum stays >= DINF.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -38,6 +44,13 @@ static_assert(RK_TIME_LIMIT < DINF, "finite values must stay below the device in
 // the splits whose two operands are older than the band.
 constexpr int32_t BAND = 16;
 
+// Splits per chunk of the band product (its operand offsets span about
+// PROD_CI * L rows from one chunk base, in 32-bit bytes).
+constexpr int32_t PROD_CI = 4;
+
+// Rows of slack before row 0 and after the infinity row of each table.
+constexpr int32_t SLACK = 32;
+
 // Per-chain arrays derived on the host (App. C quantities), resident on the device.
 struct DevChain {
     int32_t L, K;
@@ -48,15 +61,21 @@ struct DevChain {
     const int32_t *need1max;  // [L] max_o need1[s][o]: every option of block s is valid from here
     const int32_t *P;      // [L*L]  P[s*L+i] = sum_{k=s}^{i-1} r(F_k^0)        (i > s)
     const int32_t *need2;  // [L*L]  smallest m at which the sweep s..i-1 is valid (i > s)
+    int32_t xbar_halo;     // round64(max xbar): how far left case 1 reads from column m
 };
+
+// Largest case-1 shift that the finalize stages in LDS (larger ones read global memory).
+constexpr int32_t HMAX = 1024;
 
 struct Tables {
     int32_t *opt;
     int32_t *ap;
     int32_t W, stride, padl;
-    int32_t max_x;    // largest x_i over the split points; > padl means some shifts leave the row
     int64_t inf_row;  // index of the all-infinity row (= number of span rows)
 };
+
+// Rows of one table in the workspace: slack, the span rows, the infinity row, slack.
+inline int64_t table_rows(int32_t L) { return (int64_t)L * (L + 1) / 2 + 1 + 2 * SLACK; }
 
 __host__ __device__ inline int64_t row_of(int32_t L, int32_t s, int32_t t)
 {

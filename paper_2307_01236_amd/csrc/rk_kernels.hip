@@ -39,21 +39,23 @@ hipError_t Profiler::after()
 }
 
 // ---------------------------------------------------------------------------------------
-// The all-infinity row of both tables (read in place of operands that do not exist yet).
+// The all-infinity row and the slack rows of both tables (read in place of operands that
+// do not exist yet).  Block y picks the row: slack before row 0, or the infinity row and
+// the slack after it, of either table.
 // ---------------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_init_inf_rows(Tables tb)
 {
+    constexpr int32_t PER_TABLE = 2 * SLACK + 1;
     const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (j < tb.stride) {
-        tb.opt[tb.inf_row * tb.stride + j] = DINF;
-        tb.ap[tb.inf_row * tb.stride + j] = DINF;
-    }
+    const int32_t y = (int32_t)blockIdx.y, k = y % PER_TABLE;
+    const int64_t row = k < SLACK ? (int64_t)k - SLACK : tb.inf_row + (k - SLACK);
+    int32_t *const base = y < PER_TABLE ? tb.opt : tb.ap;
+    if (j < tb.stride) base[row * tb.stride + j] = DINF;
 }
 
 // ---------------------------------------------------------------------------------------
-// Raw buffer loads: a descriptor per operand block, a fixed per-lane byte offset per row.
-// Reads past the descriptor's range return 0 instead of faulting; every such read is
-// also one whose value the kernel replaces by infinity.
+// Raw buffer loads: a descriptor per operand block (its range ends with the table's slack),
+// a scalar byte offset per operand row and a fixed per-lane byte offset per column.
 // ---------------------------------------------------------------------------------------
 __device__ inline __amdgpu_buffer_rsrc_t block_rsrc(const int32_t *base, const int32_t *end)
 {
@@ -62,10 +64,6 @@ __device__ inline __amdgpu_buffer_rsrc_t block_rsrc(const int32_t *base, const i
     return __builtin_amdgcn_make_buffer_rsrc((void *)base, (short)0, (int)n, 0x00020000);
 }
 
-__device__ inline int32_t block_load(__amdgpu_buffer_rsrc_t r, uint32_t byte_off)
-{
-    return __builtin_amdgcn_raw_buffer_load_b32(r, (int)byte_off, 0, 0);
-}
 
 // ---------------------------------------------------------------------------------------
 // Workgroups of a launch go to the 8 XCDs round-robin (id g to XCD g mod 8), and each XCD
@@ -90,18 +88,36 @@ __device__ inline uint32_t xcd_tile(uint32_t g, uint32_t G)
 // and ends t = s + tau + k.  Splits are taken CI at a time.  The right operands
 // Opt(i, t, .) of a chunk, for all NQ ends of the workgroup, are staged in LDS (each
 // global row read once, then used by up to SR waves x rows); each wave reads its own left
-// operands ap(s, i).  The next chunk's operands are fetched into registers while the
-// current one is relaxed.  Operands that are not final yet or are not spans become
-// infinity; chunks where all operands are known valid skip those checks.
+// operands ap(s, i).  The next chunk's operands are loaded into registers while the
+// current one is relaxed.
+//
+// Which candidates are real: split i of cell (s,t) needs s < i <= t and both operand
+// spans below tau.  A right operand with span t - i >= tau (this also covers i <= s) is
+// replaced by infinity when staged, a left operand with span i - 1 - s >= tau (this also
+// covers i > t and splits past the workgroup's range) when used.  Both conditions are
+// thresholds in the chunk index, so only the first chunks (right) and the last ones
+// (left) mask at all.  Every other candidate that is not a split has one of these infinite
+// operands; its other operand is whatever that address holds, and the saturating unsigned
+// add keeps the sum at or above DINF.  Cells past the table's last end are computed and
+// not stored.  Addresses: one buffer descriptor per chunk and operand table; per split a
+// scalar byte offset (advanced incrementally), per row a fixed per-lane offset; all of
+// them stay inside the table with its slack rows.
 // ---------------------------------------------------------------------------------------
-template <int T>
-__global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t tau, int32_t x_fit)
+__device__ inline uint32_t sat_add(uint32_t a, uint32_t b) { return __builtin_elementwise_add_sat(a, b); }
+
+__device__ inline uint32_t buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff)
 {
-    constexpr int SR = 4, NW = 4, SW = SR * NW, CI = 4;
+    return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0);
+}
+
+template <int T>
+__global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t tau)
+{
+    constexpr int SR = 4, NW = 4, SW = SR * NW, CI = PROD_CI;
     constexpr int NQ = (SW + T - 1 + NW - 1) / NW * NW;  // staged ends, padded to the waves
     constexpr int JW = NQ / NW;                           // staged rows per wave and split
     static_assert(CI % 2 == 0, "splits are relaxed in pairs");
-    __shared__ int32_t qs[CI * NQ * 64];
+    __shared__ uint32_t qs[CI * NQ * 64];
 
     const int32_t L = ch.L;
     const uint32_t lane = threadIdx.x & 63;
@@ -114,11 +130,12 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
     const uint32_t mchunk = tile / n_rb;
     const int32_t s0 = S0 + wave * SR;
     const int64_t stride = tb.stride;
+    const int32_t padl = tb.padl;
     const uint32_t m = mchunk * 64 + lane;
-    const uint32_t colb = (uint32_t)(tb.padl + min(m, (uint32_t)tb.W - 1)) * 4u;
+    const uint32_t colb = (uint32_t)(padl + min(m, (uint32_t)tb.W - 1)) * 4u;
     const uint32_t pitch = (uint32_t)stride * 4u;
-    const int32_t *const opt_end = tb.opt + (tb.inf_row + 1) * stride;
-    const int32_t *const ap_end = tb.ap + (tb.inf_row + 1) * stride;
+    const int32_t *const opt_end = tb.opt + (tb.inf_row + 1 + SLACK) * stride;
+    const int32_t *const ap_end = tb.ap + (tb.inf_row + 1 + SLACK) * stride;
     const int32_t t0 = S0 + tau;  // first end the workgroup covers
     const int32_t i_lo = S0 + 1, i_hi = min(S0 + SW - 1 + tau, L - 1);
 
@@ -138,59 +155,44 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
         }
     }
 
-    int32_t acc[SR][T];
+    uint32_t acc[SR][T];
 #pragma unroll
     for (int r = 0; r < SR; ++r)
 #pragma unroll
         for (int k = 0; k < T; ++k) acc[r][k] = DINF;
 
-    // fetch(ic) only issues the loads of chunk ic and records, as wave-uniform bit masks,
-    // which of them are valid operands; the values are masked when they are first used
-    // (one chunk later), so the loads stay in flight while the current chunk is relaxed
-    static_assert(CI * JW <= 32 && CI * SR <= 32, "validity masks are 32-bit");
-    int32_t qv[CI][JW], av[CI][SR];
-    uint32_t qmask = 0, amask = 0;
+    // fetch(ic) issues the loads of chunk ic; their values are first used one chunk later
+    uint32_t qv[CI][JW], av[CI][SR];
     auto fetch = [&](int32_t ic) {
-        const bool q_core = x_fit && ic + CI - 1 <= i_hi && ic + CI - 1 <= t0 &&
-                            t0 + NQ - 1 - ic < tau && t0 + NQ - 1 < L;
-        const bool a_core = s0 + SR - 1 < s_end && ic >= s0 + SR && ic + CI - 1 <= s0 + tau &&
-                            ic + CI - 1 <= i_hi;
-        qmask = 0;
-        amask = 0;
+        // right operands from one row before (ic, t0): split i's rows start rel(i) rows on,
+        // shifted left by min(x_i, padl) columns (a larger x_i reads only the left pad)
+        const int32_t *const qb = tb.opt + (row_of(L, ic, t0) - 1) * stride;
+        const __amdgpu_buffer_rsrc_t rq = block_rsrc(qb, opt_end);
+        uint32_t rel = 1;
 #pragma unroll
         for (int ii = 0; ii < CI; ++ii) {
-            const int32_t i = ic + ii, ic_ = min(i, L - 1);
-            const int32_t xi = ch.x[ic_], xs = min(xi, tb.padl);
-            const int32_t *const qb = tb.opt + row_of(L, ic_, t0) * stride - xs;
-            const __amdgpu_buffer_rsrc_t rq = block_rsrc(qb, opt_end);
+            const int32_t i = ic + ii;
+            const uint32_t xs = (uint32_t)min(ch.x[min(i, L)], padl);
+            const uint32_t so = rel * pitch - 4u * xs;
 #pragma unroll
-            for (int jj = 0; jj < JW; ++jj) {
-                qv[ii][jj] = block_load(rq, qoff[jj]);
-                const int32_t t = t0 + jj * NW + wave, span = t - i;
-                const bool ok = q_core || ((i <= i_hi) & (t < L) & (span >= 0) & (span < tau) &
-                                           (xi <= tb.padl));
-                qmask |= (uint32_t)ok << (ii * JW + jj);
-            }
-            const int32_t *const ab = tb.ap + row_of(L, s0, min(i, L) - 1) * stride;
-            const __amdgpu_buffer_rsrc_t ra = block_rsrc(ab, ap_end);
-#pragma unroll
-            for (int r = 0; r < SR; ++r) {
-                av[ii][r] = block_load(ra, aoff[r]);
-                const int32_t s = s0 + r, span = i - 1 - s;
-                const bool ok = a_core || ((i <= i_hi) & (s < s_end) & (span >= 0) & (span < tau));
-                amask |= (uint32_t)ok << (ii * SR + r);
-            }
+            for (int jj = 0; jj < JW; ++jj) qv[ii][jj] = buf_load(rq, qoff[jj], so);
+            rel += (uint32_t)max(L - 1 - i, 0);
         }
+        // left operands: rows (s0 + r, ic + ii - 1), consecutive in ii
+        const int32_t *const ab = tb.ap + row_of(L, s0, ic - 1) * stride;
+        const __amdgpu_buffer_rsrc_t ra = block_rsrc(ab, ap_end);
+#pragma unroll
+        for (int ii = 0; ii < CI; ++ii)
+#pragma unroll
+            for (int r = 0; r < SR; ++r) av[ii][r] = buf_load(ra, aoff[r], (uint32_t)ii * pitch);
     };
-    constexpr uint32_t QALL = CI * JW == 32 ? 0xffffffffu : (1u << (CI * JW)) - 1u;
-    constexpr uint32_t AALL = CI * SR == 32 ? 0xffffffffu : (1u << (CI * SR)) - 1u;
 
-    const int32_t *const qw = qs + wave * SR * 64 + lane;
+    const uint32_t *const qw = qs + wave * SR * 64 + lane;
     fetch(i_lo);
     for (int32_t ic = i_lo; ic <= i_hi; ic += CI) {
-        int32_t a[CI][SR];
-        const uint32_t qm = __builtin_amdgcn_readfirstlane(qmask), am = __builtin_amdgcn_readfirstlane(amask);
-        if (qm == QALL) {
+        // staged row jj*NW + wave of split ic + ii is final iff jj*NW - ii < qlim
+        const int32_t qlim = ic - S0 - wave;
+        if (qlim > (JW - 1) * NW) {
 #pragma unroll
             for (int ii = 0; ii < CI; ++ii)
 #pragma unroll
@@ -200,14 +202,22 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
             for (int ii = 0; ii < CI; ++ii)
 #pragma unroll
                 for (int jj = 0; jj < JW; ++jj)
-                    qs[(ii * NQ + jj * NW + wave) * 64 + lane] =
-                        (qm >> (ii * JW + jj)) & 1u ? qv[ii][jj] : DINF;
+                    qs[(ii * NQ + jj * NW + wave) * 64 + lane] = jj * NW - ii < qlim ? qv[ii][jj] : DINF;
         }
+        // left operand of row r, split ic + ii is final iff r - ii > alim
+        const int32_t alim = ic - s0 - tau - 1;
+        uint32_t a[CI][SR];
+        if (alim + CI - 1 < 0) {
 #pragma unroll
-        for (int ii = 0; ii < CI; ++ii)
+            for (int ii = 0; ii < CI; ++ii)
 #pragma unroll
-            for (int r = 0; r < SR; ++r)
-                a[ii][r] = (am == AALL || ((am >> (ii * SR + r)) & 1u)) ? av[ii][r] : DINF;
+                for (int r = 0; r < SR; ++r) a[ii][r] = av[ii][r];
+        } else {
+#pragma unroll
+            for (int ii = 0; ii < CI; ++ii)
+#pragma unroll
+                for (int r = 0; r < SR; ++r) a[ii][r] = r - ii > alim ? av[ii][r] : DINF;
+        }
         __syncthreads();
         if (ic + CI <= i_hi) fetch(ic + CI);  // in flight while this chunk is relaxed
         // acc(s0+r, s0+r+tau+k) = min(acc, ap(s0+r, i) + Opt(i, s0+r+tau+k, m - x_i)), two splits per min
@@ -217,8 +227,8 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
             for (int r = 0; r < SR; ++r)
 #pragma unroll
                 for (int k = 0; k < T; ++k)
-                    acc[r][k] = min(acc[r][k], min(a[ii][r] + qw[(ii * NQ + r + k) * 64],
-                                                   a[ii + 1][r] + qw[((ii + 1) * NQ + r + k) * 64]));
+                    acc[r][k] = min(min(acc[r][k], sat_add(a[ii][r], qw[(ii * NQ + r + k) * 64])),
+                                    sat_add(a[ii + 1][r], qw[((ii + 1) * NQ + r + k) * 64]));
         __syncthreads();
     }
     if (m >= (uint32_t)tb.W) return;
@@ -227,103 +237,161 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
 #pragma unroll
         for (int k = 0; k < T; ++k) {
             const int32_t s = s0 + r, t = s + tau + k;
-            if (s < s_end && t < L) tb.opt[row_of(L, s, t) * stride + tb.padl + m] = acc[r][k];
+            if (s < s_end && t < L) tb.opt[row_of(L, s, t) * stride + padl + m] = (int32_t)acc[r][k];
         }
 }
 
 // ---------------------------------------------------------------------------------------
-// Finalize one span-length diagonal d: thread (s, m).  Adds to the band product's
-// partial minimum the splits it did not cover (one operand inside the current band:
-// max(i-1-s, t-i) >= D, D the band start) and case 1 (Eq. fe), clamps, writes Opt and
-// the row's left operand ap(s, t+1) for the spans that will split after t.
-// Row pointers advance incrementally (the ap rows of row s are consecutive; the right
-// operand row (i+1, t) is L-i-1 rows after (i, t)) and splits go four at a time so their
-// loads overlap.  A wave whose smallest budget already satisfies every option's memory
-// requirement runs case 1 without per-lane masks.
+// Finalize one span-length diagonal d: cell (s, s+d), budgets m.  Adds to the band
+// product's partial minimum the splits it did not cover (one operand inside the current
+// band: max(i-1-s, t-i) >= D, D the band start) and case 1 (Eq. fe), clamps, writes Opt
+// and the row's left operand ap(s, t+1) for the spans that will split after t.
+// A workgroup covers FC = 1024 budgets of one cell: wave w the 256 columns from
+// mbase + 256 w, lane l the four columns l, l + 64, l + 128, l + 192 of those, so every
+// scalar address serves four coalesced loads.  Splits go in batches of FB with all loads
+// of a batch issued before any is used; the row pointers of a split range advance
+// incrementally.  Case 1 reads one row, Opt(s+1, t, .), at K shifts: the workgroup stages
+// the columns it needs in LDS once (when the largest shift is at most HMAX), loading them
+// together with the first splits.
 // ---------------------------------------------------------------------------------------
-__device__ inline int32_t row_load(const int32_t *row, uint32_t byte_off)
+constexpr int32_t FC = 1024;
+
+// load at a byte offset from a wave-uniform base (one scalar base + one 32-bit lane offset)
+__device__ inline int32_t ldb(const int32_t *base, uint32_t byte_off)
 {
-    return *(const int32_t *)((const char *)row + byte_off);
+    return *(const int32_t *)((const char *)base + byte_off);
 }
 
 __global__ __launch_bounds__(256) void k_finalize(DevChain ch, Tables tb, int32_t d)
 {
-    const int32_t L = ch.L, K = ch.K;
-    const uint32_t n_mc = (uint32_t)(max(tb.W, tb.padl) + 255) / 256;
+    constexpr int32_t FB = 8, NC = 4, NST = (HMAX + FC) / 256;
+    __shared__ int32_t seg[HMAX + FC];
+    const int32_t L = ch.L, K = ch.K, W = tb.W;
+    const uint32_t n_mc = (uint32_t)(max(W, tb.padl) + FC - 1) / FC;
     const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);  // column chunks of a row adjacent
     const int32_t s = (int32_t)(tile / n_mc), t = s + d;
-    const int32_t mbase = (int32_t)(tile % n_mc) * 256;
-    const int32_t m = mbase + (int32_t)threadIdx.x;
-    const int32_t m0 = __builtin_amdgcn_readfirstlane(mbase + (int32_t)(threadIdx.x & ~63u));
+    const int32_t mbase = (int32_t)(tile % n_mc) * FC;
+    const int32_t lane = (int32_t)(threadIdx.x & 63);
+    const int32_t wave = __builtin_amdgcn_readfirstlane((int32_t)(threadIdx.x >> 6));
+    const int32_t m0 = mbase + 256 * wave;  // the wave's first column
+    const int32_t ml = m0 + lane;           // column c of the lane: ml + 64 c
     const int64_t stride = tb.stride;
     const int32_t padl = tb.padl;
-    int32_t *const orow = tb.opt + row_of(L, s, t) * stride;
-    if (m < padl) orow[m] = DINF;  // keep the left pad infinite
-    if (m >= tb.W) return;
-    const uint32_t colb = (uint32_t)(padl + m) * 4u;
+    int32_t *const orow = tb.opt + row_of(L, s, t) * stride + padl;  // column 0
     const int32_t D = (d / BAND) * BAND;
-    int32_t best = D > 0 ? row_load(orow, colb) : DINF;
 
-    // splits i in [lo, hi]: ap(s, i) + Opt(i, t, m - x_i)
-    const int32_t *const aps = tb.ap + row_of(L, s, s) * stride;  // split s+1; split i is i-1-s rows on
-    auto splits = [&](int32_t lo, int32_t hi) {
-        if (lo > hi) return;
-        const int32_t *q = tb.opt + row_of(L, lo, t) * stride;  // row (i, t)
-        int32_t i = lo;
-        auto one = [&](int32_t ii, const int32_t *qr) {
-            const int32_t xi = ch.x[ii];
-            const int32_t a = row_load(aps + (int64_t)(ii - 1 - s) * stride, colb);
-            const int32_t v = row_load(qr - min(xi, padl), colb);
-            return a + (xi <= padl ? v : DINF);
-        };
-        for (; i + 3 <= hi; i += 4) {
-            const int32_t *q1 = q + (int64_t)(L - i - 1) * stride;
-            const int32_t *q2 = q1 + (int64_t)(L - i - 2) * stride;
-            const int32_t *q3 = q2 + (int64_t)(L - i - 3) * stride;
-            const int32_t v0 = one(i, q), v1 = one(i + 1, q1), v2 = one(i + 2, q2), v3 = one(i + 3, q3);
-            best = min(best, min(min(v0, v1), min(v2, v3)));
-            q = q3 + (int64_t)(L - i - 4) * stride;
+    // case-1 row, staged: column mbase - H + q at seg[q]
+    const int32_t H = ch.xbar_halo;
+    const bool staged = d > 0 && H <= HMAX;
+    const int32_t *const rest = d > 0 ? tb.opt + row_of(L, s + 1, t) * stride + padl : nullptr;
+    int32_t stv[NST];
+    if (staged) {
+#pragma unroll
+        for (int k = 0; k < NST; ++k) {
+            const int32_t q = (int32_t)threadIdx.x + 256 * k, c = mbase - H + q;
+            stv[k] = q < H + FC && c >= -padl ? rest[c] : DINF;
         }
-        for (; i <= hi; ++i) {
-            best = min(best, one(i, q));
-            q += (int64_t)(L - i - 1) * stride;
+    }
+
+    // per-lane column offsets (past the last budget: the last one, computed and not stored)
+    uint32_t col[NC];  // byte offsets
+#pragma unroll
+    for (int c = 0; c < NC; ++c) col[c] = (uint32_t)min(ml + 64 * c, W - 1) * 4u;
+    int32_t best[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) best[c] = D > 0 ? ldb(orow, col[c]) : DINF;
+
+    // splits i0 .. i0+n-1: ap(s, i-1) + Opt(i, t, m - x_i).  Pointers at column 0:
+    // ap row (s, i-1) is i-1-s rows after (s, s); Opt row (i+1, t) is L-1-i rows after (i, t)
+    auto splits = [&](int32_t i0, int32_t n) {
+        const int32_t *pa = tb.ap + (row_of(L, s, s) + (i0 - 1 - s)) * stride + padl;
+        const int32_t *pq = tb.opt + row_of(L, i0, t) * stride + padl;
+        int32_t i = i0;
+        for (int32_t j0 = 0; j0 < n; j0 += FB) {
+            int32_t va[FB][NC], vq[FB][NC];
+#pragma unroll
+            for (int u = 0; u < FB; ++u) {
+                if (j0 + u < n) {
+                    // a shift x_i > padl happens only when padl >= W: the read lands in the left pad
+                    const int32_t *const q = pq - min(ch.x[i], padl);
+#pragma unroll
+                    for (int c = 0; c < NC; ++c) {
+                        va[u][c] = ldb(pa, col[c]);
+                        vq[u][c] = ldb(q, col[c]);
+                    }
+                    pa += stride;
+                    pq += (int64_t)(L - 1 - i) * stride;
+                    ++i;
+                } else {
+#pragma unroll
+                    for (int c = 0; c < NC; ++c) {
+                        va[u][c] = DINF;
+                        vq[u][c] = 0;
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < FB; ++u)
+#pragma unroll
+                for (int c = 0; c < NC; ++c) best[c] = min(best[c], va[u][c] + vq[u][c]);
         }
     };
     if (D == 0) {
-        splits(s + 1, t);
+        splits(s + 1, d);
     } else {
-        splits(s + 1, t - D);      // t - i >= D
-        splits(s + D + 1, t);      // i - 1 - s >= D
+        splits(s + 1, d - D);      // t - i >= D
+        splits(s + D + 1, d - D);  // i - 1 - s >= D
     }
 
     // case 1, option o: r(F_s^o) + r(B_s^o) + Opt(s+1,t,m-xbar), valid iff m >= need1[s][o]
     const int32_t *const c1 = ch.c1 + s * K, *const need1 = ch.need1 + s * K, *const xbar = ch.xbar + s * K;
     if (d == 0) {
         for (int32_t o = 0; o < K; ++o)
-            if (m >= need1[o]) best = min(best, c1[o]);
-    } else {
-        const int32_t *const rest = tb.opt + row_of(L, s + 1, t) * stride;
-        if (m0 >= ch.need1max[s]) {
-            int32_t o = 0;
-            for (; o + 3 < K; o += 4) {
-                const int32_t v0 = c1[o] + row_load(rest - xbar[o], colb);
-                const int32_t v1 = c1[o + 1] + row_load(rest - xbar[o + 1], colb);
-                const int32_t v2 = c1[o + 2] + row_load(rest - xbar[o + 2], colb);
-                const int32_t v3 = c1[o + 3] + row_load(rest - xbar[o + 3], colb);
-                best = min(best, min(min(v0, v1), min(v2, v3)));
-            }
-            for (; o < K; ++o) best = min(best, c1[o] + row_load(rest - xbar[o], colb));
-        } else {
-            for (int32_t o = 0; o < K; ++o)
-                if (m >= need1[o]) best = min(best, c1[o] + row_load(rest - xbar[o], colb));
+#pragma unroll
+            for (int c = 0; c < NC; ++c)
+                if (ml + 64 * c >= need1[o]) best[c] = min(best[c], c1[o]);
+    } else if (staged) {
+#pragma unroll
+        for (int k = 0; k < NST; ++k) {
+            const int32_t q = (int32_t)threadIdx.x + 256 * k;
+            if (q < H + FC) seg[q] = stv[k];
         }
+        __syncthreads();
+        const int32_t *const sg = seg + H + (ml - mbase);  // column ml
+        if (m0 >= ch.need1max[s]) {
+            for (int32_t o = 0; o < K; ++o) {
+                const int32_t *const so = sg - xbar[o];
+#pragma unroll
+                for (int c = 0; c < NC; ++c) best[c] = min(best[c], c1[o] + so[64 * c]);
+            }
+        } else {
+            for (int32_t o = 0; o < K; ++o) {
+                const int32_t *const so = sg - xbar[o];
+#pragma unroll
+                for (int c = 0; c < NC; ++c)
+                    if (ml + 64 * c >= need1[o]) best[c] = min(best[c], c1[o] + so[64 * c]);
+            }
+        }
+    } else {
+        for (int32_t o = 0; o < K; ++o)
+#pragma unroll
+            for (int c = 0; c < NC; ++c)
+                if (ml + 64 * c >= need1[o]) best[c] = min(best[c], c1[o] + ldb(rest - xbar[o], col[c]));
     }
-    best = min(best, DINF);
-    orow[padl + m] = best;
-    if (t + 1 < L) {
-        const int32_t i = t + 1;
-        tb.ap[row_of(L, s, t) * stride + padl + m] =
-            m >= ch.need2[s * L + i] ? min(ch.P[s * L + i] + best, DINF) : DINF;
+
+    // stores last: until here every scalar operand may come from the scalar cache
+    int32_t *const arow = tb.ap + row_of(L, s, t) * stride + padl;
+    const int32_t ip = t + 1 < L ? s * L + t + 1 : 0;
+    const int32_t need2 = t + 1 < L ? ch.need2[ip] : 0, P = t + 1 < L ? ch.P[ip] : 0;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        const int32_t m = ml + 64 * c;
+        if (m < padl) orow[m - padl] = DINF;  // keep the left pad infinite
+        if (m < W) {
+            const int32_t v = min(best[c], DINF);
+            orow[m] = v;
+            if (t + 1 < L) arow[m] = m >= need2 ? min(P + v, DINF) : DINF;
+        }
     }
 }
 
@@ -333,17 +401,17 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
     hipError_t e;
     int32_t n = 0;
     if ((e = prof->before(KFILL_INIT)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_init_inf_rows, dim3((tb.stride + 255) / 256), dim3(256), 0, stream, tb);
+    hipLaunchKernelGGL(k_init_inf_rows, dim3((tb.stride + 255) / 256, 2 * (2 * SLACK + 1)), dim3(256), 0,
+                       stream, tb);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = prof->after()) != hipSuccess) return e;
     ++n;
-    const int32_t fin_x = (max(tb.W, tb.padl) + 255) / 256;
+    const int32_t fin_x = (max(tb.W, tb.padl) + FC - 1) / FC;
     for (int32_t d = 0; d < ch.L; ++d) {
         if (d > 0 && d % BAND == 0) {
             const dim3 grid(((tb.W + 63) / 64) * ((ch.L - d + 15) / 16));
             if ((e = prof->before(KFILL_PRODUCT)) != hipSuccess) return e;
-            hipLaunchKernelGGL((k_product<BAND>), grid, dim3(256), 0, stream, ch, tb, d,
-                               (int32_t)(tb.max_x <= tb.padl));
+            hipLaunchKernelGGL((k_product<BAND>), grid, dim3(256), 0, stream, ch, tb, d);
             if ((e = hipGetLastError()) != hipSuccess) return e;
             if ((e = prof->after()) != hipSuccess) return e;
             ++n;

@@ -99,9 +99,10 @@ def test_workspace_bytes():
     ch = make_config_chain(4)
     h = rk.rk_chain_create(*_args(ch))
     try:
-        # two tables (Opt and the case-2 left operand), each with one extra all-infinity row;
-        # rows are a 64-column infinity pad (max x_i = 7 here) plus the budget columns
-        rows = ch.L * (ch.L + 1) // 2 + 1
+        # two tables (Opt and the case-2 left operand), each with one extra all-infinity row
+        # and 32 rows of slack at either end; rows are a 64-column infinity pad (max x_i = 7
+        # here) plus the budget columns
+        rows = ch.L * (ch.L + 1) // 2 + 1 + 64
         assert rk.rk_workspace_bytes(h, 6000) == 2 * rows * (64 + 6016) * 4
         assert rk.rk_workspace_bytes(h, 0) == 2 * rows * (64 + 64) * 4
         with pytest.raises(rk.RKError):
