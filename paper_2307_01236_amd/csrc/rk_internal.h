@@ -41,8 +41,11 @@ constexpr int32_t DINF = (1 << 30) - 1;
 static_assert(RK_TIME_LIMIT < DINF, "finite values must stay below the device infinity");
 
 // Spans per band: every band of BAND span lengths gets one tiled product over
-// the splits whose two operands are older than the band.
-constexpr int32_t BAND = 16;
+// the splits whose two operands are older than the band.  Inside a band, mid
+// products every MIDMIN spans cover the splits whose longer operand lies in the
+// band's earlier part, so that a diagonal's own launch adds fewer than 2 MIDMIN.
+constexpr int32_t BAND = 32;
+constexpr int32_t MIDMIN = 8;
 
 // Splits per chunk of the band product (its operand offsets span about
 // PROD_CI * L rows from one chunk base, in 32-bit bytes).
@@ -105,7 +108,7 @@ struct Profiler {
 };
 
 // Kernel kinds of the fill, in the order rk_fill_kernel_stats reports them.
-enum FillKernel : int32_t { KFILL_PRODUCT = 0, KFILL_FINALIZE, KFILL_INIT, KFILL_NKINDS };
+enum FillKernel : int32_t { KFILL_PRODUCT = 0, KFILL_MID, KFILL_FINALIZE, KFILL_INIT, KFILL_NKINDS };
 static_assert(KFILL_NKINDS <= 8, "Profiler::work holds 8 kinds");
 extern const char *const kFillKernelNames[KFILL_NKINDS];
 

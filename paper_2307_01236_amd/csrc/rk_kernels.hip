@@ -13,9 +13,11 @@
 // attains Opt(s,t,m)), so the fill keeps no argmin bookkeeping.
 #include "rk_internal.h"
 
+#include <type_traits>
+
 namespace rk {
 
-const char *const kFillKernelNames[KFILL_NKINDS] = {"k_product", "k_finalize", "k_init_inf_rows"};
+const char *const kFillKernelNames[KFILL_NKINDS] = {"k_product", "k_mid", "k_finalize", "k_init_inf_rows"};
 
 hipError_t Profiler::before(int32_t kind)
 {
@@ -83,7 +85,7 @@ __device__ inline uint32_t xcd_tile(uint32_t g, uint32_t G)
 // the splits i whose two operands are older than the band (both s..i-1 and i..t shorter
 // than tau).  That is a min-plus product, elementwise in m:
 //     acc(s,t) = min_i ap(s,i) + Opt(i, t, m - x_i).
-// A workgroup owns 64 consecutive budgets (lane = m) and SW = 16 consecutive rows s; its
+// A workgroup owns 64 consecutive budgets (lane = m) and SW = 4 SR consecutive rows s; its
 // wave w keeps, per lane, the SR x T accumulators of rows s0..s0+SR-1 (s0 = S0 + SR w)
 // and ends t = s + tau + k.  Splits are taken CI at a time.  The right operands
 // Opt(i, t, .) of a chunk, for all NQ ends of the workgroup, are staged in LDS (each
@@ -110,10 +112,10 @@ __device__ inline uint32_t buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uin
     return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0);
 }
 
-template <int T>
+template <int SR, int T>
 __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t tau)
 {
-    constexpr int SR = 4, NW = 4, SW = SR * NW, CI = PROD_CI;
+    constexpr int NW = 4, SW = SR * NW, CI = PROD_CI;
     constexpr int NQ = (SW + T - 1 + NW - 1) / NW * NW;  // staged ends, padded to the waves
     constexpr int JW = NQ / NW;                           // staged rows per wave and split
     static_assert(CI % 2 == 0, "splits are relaxed in pairs");
@@ -242,9 +244,178 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
 }
 
 // ---------------------------------------------------------------------------------------
-// Finalize one span-length diagonal d: cell (s, s+d), budgets m.  Adds to the band
-// product's partial minimum the splits it did not cover (one operand inside the current
-// band: max(i-1-s, t-i) >= D, D the band start) and case 1 (Eq. fe), clamps, writes Opt
+// Mid product of width WD inside a band.  For the spans d in [tau, tau + WD), lo = tau - WD,
+// the part of Eq. fn over the splits whose longer operand has a span in [lo, tau):
+//   group A: left span a = i-1-s in [lo, tau) (the right span d-1-a is then below 2 WD - 1)
+//   group B: right span b = t-i in [lo, tau) (the left span is then below 2 WD - 1)
+// Every lo > 0 used is at least 2 WD, so the groups are disjoint and their short operand
+// spans lie below lo.  With lo == 0 the launch covers the splits whose two spans are both
+// below WD (group A with the right span bounded too).  These are splits that one finalize
+// launch per diagonal would otherwise read operand by operand.
+// The two groups are separate launches (both write every cell of the spans, the second
+// one taking the minimum with what the first stored).
+// A wave owns R = 4 rows (group A: rows s0 + r, ends s0 + r + tau + k) or R ends (group B:
+// ends t0 + r, rows t0 + r - tau - k), k < WD, and 64 budgets.  The tile's WD + R - 1
+// splits are unrolled; which (split, row) pairs are real depends only on their positions
+// in the tile, so it is known at compile time and nothing is masked.  A split's operand
+// loads are issued one split ahead of its relaxation.  Cells past the table are computed
+// and not stored (their operand rows are clamped into the table).
+// ---------------------------------------------------------------------------------------
+// Calls f(integral_constant<int, U>) for U = B .. E-1 in order: a loop unrolled by
+// construction, whose index is a compile-time constant in the body.
+template <int B, int E, typename F>
+__device__ inline void static_for(F &&f)
+{
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
+    }
+}
+
+template <int WD, bool GA, bool LO0>
+__global__ __launch_bounds__(256) void k_mid(DevChain ch, Tables tb, int32_t tau, int32_t accumulate)
+{
+    constexpr int R = 4, NS = WD + R - 1, NJ = R + WD - 1;
+    static_assert(WD == 8 || WD == 16, "widths 8 and 16");
+    static_assert(GA || !LO0, "lo == 0 is group A only");
+    const int32_t L = ch.L, W = tb.W, lo = tau - WD;
+    const int32_t lane = (int32_t)(threadIdx.x & 63);
+    const int32_t wave = __builtin_amdgcn_readfirstlane((int32_t)(threadIdx.x >> 6));
+    const int32_t n_blk = (L - tau + R - 1) / R;  // row blocks (A), end blocks (B)
+    const int32_t n_mc = (W + 63) / 64;
+    const int32_t g = (int32_t)xcd_tile(blockIdx.x, gridDim.x) * 4 + wave;
+    if (g >= n_blk * n_mc) return;
+    const int32_t mc = g / n_blk, blk = g % n_blk;
+    const int64_t stride = tb.stride;
+    const uint32_t pitch = (uint32_t)stride * 4u;
+    const int32_t padl = tb.padl;
+    const int32_t m = mc * 64 + lane;
+    const uint32_t col = (uint32_t)(padl + min(m, W - 1)) * 4u;
+    const int32_t *const opt_end = tb.opt + (tb.inf_row + 1 + SLACK) * stride;
+    const int32_t *const ap_end = tb.ap + (tb.inf_row + 1 + SLACK) * stride;
+    auto rows_between = [&](int32_t s_from, int32_t s_to) {  // row(s_to, t) - row(s_from, t)
+        return (int64_t)(s_to - s_from) * (L - 1) - ((int64_t)s_to * (s_to - 1) - (int64_t)s_from * (s_from - 1)) / 2;
+    };
+
+    uint32_t acc[R][WD];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int k = 0; k < WD; ++k) acc[r][k] = DINF;
+
+    // Operand r of a split: group A the left operand of row s0 + r, group B the right
+    // operand of end t0 + r.  Operand j: group A the right operand of end s0 + tau + j,
+    // group B the left operand of row t0 - tau - WD + 1 + j (rows below 0 clamped to 0).
+    uint32_t xoff[NJ], roff[R];
+    const int32_t base = blk * R;                // s0 (A) or t0 - tau (B)
+    int32_t i = GA ? base + lo + 1 : base + 1;   // the tile's first split
+    int64_t rq, ra;  // Opt row (i, first end) and ap row (first row, i - 1) of the current split
+    if (GA) {
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) xoff[j] = (uint32_t)j * pitch + col;
+#pragma unroll
+        for (int r = 0; r < R; ++r) roff[r] = (uint32_t)rows_between(base, min(base + r, L - 1)) * pitch + col;
+        rq = row_of(L, i, base + tau);
+        ra = row_of(L, base, i - 1);
+    } else {
+        const int32_t sb = base - WD + 1, sc0 = max(sb, 0);
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) xoff[j] = (uint32_t)rows_between(sc0, max(sb + j, 0)) * pitch + col;
+#pragma unroll
+        for (int r = 0; r < R; ++r) roff[r] = (uint32_t)r * pitch + col;
+        rq = row_of(L, i, base + tau);
+        ra = row_of(L, sc0, i - 1);
+    }
+
+    uint32_t vr[2][R], vj[2][NJ];
+    // split u is real for operand r in [u - WD + 1, u]; operand j is needed in [rlo, rhi + WD - 1]
+    auto load = [&](auto uc) {
+        constexpr int u = decltype(uc)::value, b = u & 1;
+        constexpr int rlo = u - WD + 1 > 0 ? u - WD + 1 : 0, rhi = u < R - 1 ? u : R - 1;
+        constexpr int jhi = LO0 ? (rhi + WD - 1 < u ? rhi + WD - 1 : u) : rhi + WD - 1;
+        // a shift x_i > padl happens only when padl >= W: the read lands in the left pad
+        const int32_t xs = min(ch.x[min(i, L - 1)], padl);
+        const __amdgpu_buffer_rsrc_t dq = block_rsrc(tb.opt + rq * stride - xs, opt_end);
+        const __amdgpu_buffer_rsrc_t da = block_rsrc(tb.ap + ra * stride, ap_end);
+#pragma unroll
+        for (int r = rlo; r <= rhi; ++r) vr[b][r] = buf_load(GA ? da : dq, roff[r], 0);
+#pragma unroll
+        for (int j = rlo; j <= jhi; ++j) vj[b][j] = buf_load(GA ? dq : da, xoff[j], 0);
+        // next split: Opt row (i+1, t) is L-1-i rows after (i, t); ap rows advance by one
+        rq += max(L - 1 - i, 0);
+        ra += 1;
+        ++i;
+    };
+    auto relax = [&](auto uc) {
+        constexpr int u = decltype(uc)::value, b = u & 1;
+        constexpr int rlo = u - WD + 1 > 0 ? u - WD + 1 : 0, rhi = u < R - 1 ? u : R - 1;
+#pragma unroll
+        for (int r = rlo; r <= rhi; ++r)
+#pragma unroll
+            for (int k = 0; k < WD; ++k) {
+                if (GA) {
+                    if (!LO0 || r + k <= u)  // with lo == 0 the right span stays below WD
+                        acc[r][k] = min(acc[r][k], sat_add(vr[b][r], vj[b][r + k]));
+                } else {
+                    acc[r][k] = min(acc[r][k], sat_add(vj[b][r - k + WD - 1], vr[b][r]));
+                }
+            }
+    };
+    load(std::integral_constant<int, 0>{});
+    static_for<0, NS>([&](auto uc) {
+        constexpr int u = decltype(uc)::value;
+        if constexpr (u + 1 < NS) load(std::integral_constant<int, u + 1>{});
+        relax(uc);
+        // the accumulators are final for this split here, and nothing moves across: only
+        // one split's operands are held in registers ahead of their use
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            if constexpr (WD == 16)
+                asm volatile("" ::"v"(acc[r][0]), "v"(acc[r][1]), "v"(acc[r][2]), "v"(acc[r][3]), "v"(acc[r][4]),
+                             "v"(acc[r][5]), "v"(acc[r][6]), "v"(acc[r][7]), "v"(acc[r][8]), "v"(acc[r][9]),
+                             "v"(acc[r][10]), "v"(acc[r][11]), "v"(acc[r][12]), "v"(acc[r][13]), "v"(acc[r][14]),
+                             "v"(acc[r][15]));
+            else
+                asm volatile("" ::"v"(acc[r][0]), "v"(acc[r][1]), "v"(acc[r][2]), "v"(acc[r][3]), "v"(acc[r][4]),
+                             "v"(acc[r][5]), "v"(acc[r][6]), "v"(acc[r][7]));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    });
+
+    // store (or fold into the stored partial) through one descriptor per row r: group A
+    // cell (s0+r, s0+r+tau+k) is k rows after (s0+r, s0+r+tau); group B cell
+    // (t0+r-tau-k, t0+r) is sum_{s'=t0+r-tau-k}^{t0+r-tau-1} (L-1-s') rows before (t0+r-tau, t0+r)
+    if (m >= W) return;
+    const uint32_t cst = (uint32_t)(padl + m) * 4u;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int32_t sr = base + r;  // group A: the row; group B: the row of span tau at end t0 + r
+        const int32_t tr = base + r + tau;
+        if (sr < L - tau) {  // some cell of this row (A) or end (B) lies in the table
+            int32_t *const rb = tb.opt + row_of(L, sr, tr) * stride;
+            int64_t back = 0;  // group B: rows from (sr - k, tr) to (sr, tr)
+#pragma unroll
+            for (int k = 0; k < WD; ++k) {
+                if (!GA && k > 0) back += L - 1 - (sr - k);
+                if (GA ? tr + k < L : sr - k >= 0) {
+                    int32_t *const p = GA ? rb + (int64_t)k * stride : rb - back * stride;
+                    const __amdgpu_buffer_rsrc_t dr =
+                        __builtin_amdgcn_make_buffer_rsrc(p, (short)0, (int)pitch, 0x00020000);
+                    uint32_t v = acc[r][k];
+                    if (accumulate) v = min(v, (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(dr, (int)cst, 0, 0));
+                    __builtin_amdgcn_raw_buffer_store_b32((int)v, dr, (int)cst, 0, 0);
+                }
+            }
+        }
+    }
+}
+
+
+
+// ---------------------------------------------------------------------------------------
+// Finalize one span-length diagonal d: cell (s, s+d), budgets m.  Adds to the products'
+// partial minimum the splits they did not cover (max(i-1-s, t-i) >= D, D = d rounded down
+// to a multiple of MIDMIN) and case 1 (Eq. fe), clamps, writes Opt
 // and the row's left operand ap(s, t+1) for the spans that will split after t.
 // A workgroup covers FC = 1024 budgets of one cell: wave w the 256 columns from
 // mbase + 256 w, lane l the four columns l, l + 64, l + 128, l + 192 of those, so every
@@ -262,6 +433,14 @@ __device__ inline int32_t ldb(const int32_t *base, uint32_t byte_off)
     return *(const int32_t *)((const char *)base + byte_off);
 }
 
+// the same through a buffer descriptor of one row (bytes [0, pitch) from base): the lane
+// offset goes to the load unchanged, with no per-lane address arithmetic
+__device__ inline int32_t ldrow(const int32_t *base, uint32_t pitch, uint32_t byte_off)
+{
+    const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc((void *)base, (short)0, (int)pitch, 0x00020000);
+    return __builtin_amdgcn_raw_buffer_load_b32(r, (int)byte_off, 0, 0);
+}
+
 __global__ __launch_bounds__(256) void k_finalize(DevChain ch, Tables tb, int32_t d)
 {
     constexpr int32_t FB = 8, NC = 4, NST = (HMAX + FC) / 256;
@@ -276,9 +455,10 @@ __global__ __launch_bounds__(256) void k_finalize(DevChain ch, Tables tb, int32_
     const int32_t m0 = mbase + 256 * wave;  // the wave's first column
     const int32_t ml = m0 + lane;           // column c of the lane: ml + 64 c
     const int64_t stride = tb.stride;
+    const uint32_t pitch = (uint32_t)stride * 4u;
     const int32_t padl = tb.padl;
     int32_t *const orow = tb.opt + row_of(L, s, t) * stride + padl;  // column 0
-    const int32_t D = (d / BAND) * BAND;
+    const int32_t D = (d / MIDMIN) * MIDMIN;  // the products cover splits with max(a, b) < D
 
     // case-1 row, staged: column mbase - H + q at seg[q]
     const int32_t H = ch.xbar_halo;
@@ -316,8 +496,8 @@ __global__ __launch_bounds__(256) void k_finalize(DevChain ch, Tables tb, int32_
                     const int32_t *const q = pq - min(ch.x[i], padl);
 #pragma unroll
                     for (int c = 0; c < NC; ++c) {
-                        va[u][c] = ldb(pa, col[c]);
-                        vq[u][c] = ldb(q, col[c]);
+                        va[u][c] = ldrow(pa, pitch, col[c]);
+                        vq[u][c] = ldrow(q, pitch, col[c]);
                     }
                     pa += stride;
                     pq += (int64_t)(L - 1 - i) * stride;
@@ -395,9 +575,52 @@ __global__ __launch_bounds__(256) void k_finalize(DevChain ch, Tables tb, int32_
     }
 }
 
+// Relaxations (real split candidates) one product launch covers: cells of spans dd in
+// [tau, tau + T) whose split has a left span a and a right span dd-1-a in the given windows.
+static int64_t product_work(int32_t L, int32_t W, int32_t tau, int32_t T, int32_t alo, int32_t ahi,
+                            int32_t blo, int32_t bhi)
+{
+    int64_t n = 0;
+    for (int32_t dd = tau; dd < min(tau + T, L); ++dd) {
+        int64_t c = 0;
+        for (int32_t a = alo; a < min(ahi, dd); ++a) c += (dd - 1 - a >= blo && dd - 1 - a < bhi);
+        n += (int64_t)(L - dd) * c;
+    }
+    return n * W;
+}
+
+template <int WD>
+static hipError_t launch_mid(const DevChain &ch, const Tables &tb, hipStream_t stream, int32_t d,
+                             int32_t *n, Profiler *prof)
+{
+    hipError_t e;
+    const int32_t lo = d - WD;
+    const int32_t n_blk = (ch.L - d + 3) / 4, n_mc = (tb.W + 63) / 64;
+    const dim3 grid((n_blk * n_mc + 3) / 4);
+    for (int32_t group = 0; group < (lo == 0 ? 1 : 2); ++group) {
+        if ((e = prof->before(KFILL_MID)) != hipSuccess) return e;
+        if (lo == 0)
+            hipLaunchKernelGGL((k_mid<WD, true, true>), grid, dim3(256), 0, stream, ch, tb, d, 0);
+        else if (group == 0)
+            hipLaunchKernelGGL((k_mid<WD, true, false>), grid, dim3(256), 0, stream, ch, tb, d, 1);
+        else
+            hipLaunchKernelGGL((k_mid<WD, false, false>), grid, dim3(256), 0, stream, ch, tb, d, 1);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = prof->after()) != hipSuccess) return e;
+        ++*n;
+    }
+    prof->work[KFILL_MID] += lo == 0 ? product_work(ch.L, tb.W, d, WD, 0, WD, 0, WD)
+                                     : product_work(ch.L, tb.W, d, WD, lo, d, 0, d) +
+                                           product_work(ch.L, tb.W, d, WD, 0, lo, lo, d);
+    return hipSuccess;
+}
+
+// The fill: per diagonal d, the products that complete before it (a band product every
+// BAND spans, mid products in between down to MIDMIN), then its finalize.
 hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream, int32_t *launches,
                        Profiler *prof)
 {
+    static_assert(BAND == 32 && MIDMIN == 8, "the launch sequence below is written for these");
     hipError_t e;
     int32_t n = 0;
     if ((e = prof->before(KFILL_INIT)) != hipSuccess) return e;
@@ -409,22 +632,25 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
     const int32_t fin_x = (max(tb.W, tb.padl) + FC - 1) / FC;
     for (int32_t d = 0; d < ch.L; ++d) {
         if (d > 0 && d % BAND == 0) {
-            const dim3 grid(((tb.W + 63) / 64) * ((ch.L - d + 15) / 16));
+            constexpr int SR = 2, SW = 4 * SR;
+            const dim3 grid(((tb.W + 63) / 64) * ((ch.L - d + SW - 1) / SW));
             if ((e = prof->before(KFILL_PRODUCT)) != hipSuccess) return e;
-            hipLaunchKernelGGL((k_product<BAND>), grid, dim3(256), 0, stream, ch, tb, d);
+            hipLaunchKernelGGL((k_product<SR, BAND>), grid, dim3(256), 0, stream, ch, tb, d);
             if ((e = hipGetLastError()) != hipSuccess) return e;
             if ((e = prof->after()) != hipSuccess) return e;
             ++n;
-            // splits with both operands shorter than d: 2d - d' of them for a cell of span d'
-            for (int32_t dd = d; dd < min(d + BAND, ch.L); ++dd)
-                prof->work[KFILL_PRODUCT] += (int64_t)(ch.L - dd) * (2 * d - dd) * tb.W;
+            prof->work[KFILL_PRODUCT] += product_work(ch.L, tb.W, d, BAND, 0, d, 0, d);
+        } else if (d % 16 == 0 && d > 0) {
+            if ((e = launch_mid<16>(ch, tb, stream, d, &n, prof)) != hipSuccess) return e;
+        } else if (d % 8 == 0 && d > 0) {
+            if ((e = launch_mid<8>(ch, tb, stream, d, &n, prof)) != hipSuccess) return e;
         }
         if ((e = prof->before(KFILL_FINALIZE)) != hipSuccess) return e;
         hipLaunchKernelGGL(k_finalize, dim3(fin_x * (ch.L - d)), dim3(256), 0, stream, ch, tb, d);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if ((e = prof->after()) != hipSuccess) return e;
         ++n;
-        const int32_t D = (d / BAND) * BAND;
+        const int32_t D = (d / MIDMIN) * MIDMIN;
         prof->work[KFILL_FINALIZE] += (int64_t)(ch.L - d) * ((D > 0 ? 2 * (d - D) : d) + ch.K) * tb.W;
     }
     *launches = n;
