@@ -189,9 +189,25 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
             for (int r = 0; r < SR; ++r) av[ii][r] = buf_load(ra, aoff[r], (uint32_t)ii * pitch);
     };
 
+    // Chunk order: neighbouring row blocks share most right operand rows at equal split i,
+    // so the row blocks of a group start at one common split (anchor) and wrap around:
+    // [anchor, i_hi] in order, then [i_lo, anchor).  Their ranges differ by a shift only,
+    // so after the wrap they again visit equal i at about equal times, and the rows they
+    // share are read from L2 while still there.  (A chunk of the second part may run into
+    // the anchor: its splits are relaxed twice, which leaves the minimum unchanged.)
+    const int32_t gspan = (tau + 2 * SW - 2) / SW * SW;  // rows of a group
+    int32_t anchor = S0 / gspan * gspan + gspan - SW + 1;
+    if (anchor > i_hi) anchor = i_lo;
+    constexpr int32_t DONE = 0x7fffffff;
+    auto next_chunk = [&](int32_t c) {
+        if (c >= anchor) return c + CI <= i_hi ? c + CI : (i_lo < anchor ? i_lo : DONE);
+        return c + CI < anchor ? c + CI : DONE;
+    };
+
     const uint32_t *const qw = qs + wave * SR * 64 + lane;
-    fetch(i_lo);
-    for (int32_t ic = i_lo; ic <= i_hi; ic += CI) {
+    fetch(anchor);
+    for (int32_t ic = anchor; ic != DONE;) {
+        const int32_t inext = next_chunk(ic);
         // staged row jj*NW + wave of split ic + ii is final iff jj*NW - ii < qlim
         const int32_t qlim = ic - S0 - wave;
         if (qlim > (JW - 1) * NW) {
@@ -221,7 +237,7 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
                 for (int r = 0; r < SR; ++r) a[ii][r] = r - ii > alim ? av[ii][r] : DINF;
         }
         __syncthreads();
-        if (ic + CI <= i_hi) fetch(ic + CI);  // in flight while this chunk is relaxed
+        if (inext != DONE) fetch(inext);  // in flight while this chunk is relaxed
         // acc(s0+r, s0+r+tau+k) = min(acc, ap(s0+r, i) + Opt(i, s0+r+tau+k, m - x_i)), two splits per min
 #pragma unroll
         for (int ii = 0; ii < CI; ii += 2)
@@ -232,6 +248,7 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
                     acc[r][k] = min(min(acc[r][k], sat_add(a[ii][r], qw[(ii * NQ + r + k) * 64])),
                                     sat_add(a[ii + 1][r], qw[((ii + 1) * NQ + r + k) * 64]));
         __syncthreads();
+        ic = inext;
     }
     if (m >= (uint32_t)tb.W) return;
 #pragma unroll
