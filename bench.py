@@ -9,10 +9,13 @@ the solve runs on a torch stream.
 
 Prints one JSON line on stdout.  ``value`` is DP relaxations per second of
 the whole step (relaxations = candidate evaluations of the recurrence,
-(M+1) * sum_d (L-d)(K+d)).  ``roofline`` reports the dominant fill kernel
-against the VALU integer peak, from per-launch HIP events on the solve's
-stream.  ``cpu_baseline`` times the CPU oracle (one core) on a bounded part of
-the same chain.
+(M+1) * sum_d (L-d)(K+d)).  ``roofline`` reports the dominant fill kernel (the
+kind with the most device time, from per-launch HIP events on the solve's
+stream) against the roof that binds it: HBM bandwidth for its compulsory table
+traffic (every row a launch reads counted once, plus the rows it writes) or the
+VALU integer peak for its relaxations (an add and a min each), whichever
+fraction is higher; the other one is reported beside it.  ``cpu_baseline``
+times the CPU oracle (one core) on a bounded part of the same chain.
 """
 from __future__ import annotations
 
@@ -143,11 +146,12 @@ def main():
     kern = {}
     for i in range(args.steps):
         step()
-        for name, (n, ms, work) in s.kernel_stats().items():
-            a = kern.setdefault(name, [0, 0.0, 0])
+        for name, (n, ms, work, moved) in s.kernel_stats().items():
+            a = kern.setdefault(name, [0, 0.0, 0, 0])
             a[0] += n
             a[1] += ms
             a[2] += work
+            a[3] += moved
     s.set_profiling(False)
 
     # solve wall time without the schedule, warm (synchronous rk_solve on the library's table)
@@ -160,25 +164,26 @@ def main():
     s.schedule()
     sched_ms = (time.perf_counter() - t) * 1e3
 
-    # dominant kernel: the one with the most device time; its algorithmic work is the
-    # relaxations it performs (2 int32 ops each: an add and a min)
-    dname, (dn, dms, dwork) = max(kern.items(), key=lambda kv: kv[1][1])
-    per_launch_ms = dms / dn
+    # dominant kernel: the one with the most device time; both of its roofs per launch
+    dname, (dn, dms, dwork, dbytes) = max(kern.items(), key=lambda kv: kv[1][1])
+    per_launch_s = dms / dn * 1e-3
     ops_per_launch = OPS_PER_RELAX * dwork / dn
-    achieved_tops = ops_per_launch / (per_launch_ms * 1e-3) / 1e12
-    traffic, hbm_frac = measured_traffic(ch.name, dname)
-    if traffic is not None:
-        hbm_frac = traffic / (per_launch_ms * 1e-3) / (HBM_PEAK_GBS * 1e9)
-    roofline = {
-        "bound": "alu", "kernel": dname,
-        "achieved": achieved_tops, "peak": VALU_PEAK_TOPS, "unit": "TOP/s",
-        "frac": achieved_tops / VALU_PEAK_TOPS,
-        "traffic": traffic, "traffic_hbm_frac": hbm_frac,
-        "launches_per_step": dn / args.steps, "avg_launch_ms": per_launch_ms,
-        "ops_per_launch": ops_per_launch,
-        "whole_fill_frac": OPS_PER_RELAX * relax / (statistics.median(fill_ms) * 1e-3) / 1e12
-                           / VALU_PEAK_TOPS,
-    }
+    bytes_per_launch = dbytes / dn
+    valu = {"bound": "alu", "achieved": ops_per_launch / per_launch_s / 1e12, "peak": VALU_PEAK_TOPS,
+            "unit": "TOP/s", "work_per_launch": ops_per_launch}
+    valu["frac"] = valu["achieved"] / VALU_PEAK_TOPS
+    hbm = {"bound": "hbm", "achieved": bytes_per_launch / per_launch_s / 1e9, "peak": HBM_PEAK_GBS,
+           "unit": "GB/s", "work_per_launch": bytes_per_launch}
+    hbm["frac"] = hbm["achieved"] / HBM_PEAK_GBS
+    bind, other = (hbm, valu) if hbm["frac"] >= valu["frac"] else (valu, hbm)
+    traffic, _ = measured_traffic(ch.name, dname)
+    roofline = dict(bind)
+    roofline.update({
+        "traffic": traffic, "kernel": dname, "launches_per_step": dn / args.steps,
+        "avg_launch_ms": dms / dn, "other_roof": other,
+        "whole_fill_valu_frac": OPS_PER_RELAX * relax / (statistics.median(fill_ms) * 1e-3) / 1e12
+                                / VALU_PEAK_TOPS,
+    })
 
     cpu = None
     if args.cpu_blocks > 0:
@@ -198,7 +203,7 @@ def main():
         "fill_relax_per_s": relax / (statistics.median(fill_ms) * 1e-3),
         "roofline": roofline, "cpu_baseline": cpu,
         "kernels": {k: {"launches_per_step": v[0] / args.steps, "ms_per_step": v[1] / args.steps,
-                        "relaxations_per_step": v[2] // args.steps}
+                        "relaxations_per_step": v[2] // args.steps, "table_bytes_per_step": v[3] // args.steps}
                     for k, v in kern.items()},
     }
     s.close()

@@ -151,15 +151,18 @@ int rk_last_fill_ms(rk_chain *c, float *ms, int32_t *launches);
  * stream, and the fill launches its kernels one by one instead of replaying a
  * graph.  rk_fill_kernel_stats then reports, for kernel kind `kind`
  * (0 <= kind < *n_kinds), its name as a profiler shows it, the number of its
- * launches in the last solve, their summed device time in milliseconds and the
+ * launches in the last solve, their summed device time in milliseconds, the
  * number of candidate evaluations of the recurrence (relaxations, counting
- * only valid (s,t,m,choice) combinations) those launches performed.  Any
- * output pointer may be NULL.  Waits for the last solve; timings need
- * profiling to have been on during it.  RK_E_INVAL for a kind out of range.
+ * only valid (s,t,m,choice) combinations) those launches performed, and their
+ * compulsory table traffic in bytes: every table row a launch reads counted
+ * once, its budget columns only, plus every row it writes (and reads back, where
+ * it folds into a stored partial).  Any output pointer may be NULL.  Waits for
+ * the last solve; timings need profiling to have been on during it.
+ * RK_E_INVAL for a kind out of range.
  */
 int rk_set_profiling(rk_chain *c, int32_t enable);
 int rk_fill_kernel_stats(rk_chain *c, int32_t kind, int32_t *n_kinds, const char **name,
-                         int32_t *launches, float *total_ms, int64_t *relaxations);
+                         int32_t *launches, float *total_ms, int64_t *relaxations, int64_t *bytes);
 
 /* Short English description of an RK_* code. */
 const char *rk_strerror(int code);

@@ -443,7 +443,7 @@ int rk_set_profiling(rk_chain *c, int32_t enable)
 }
 
 int rk_fill_kernel_stats(rk_chain *c, int32_t kind, int32_t *n_kinds, const char **name,
-                         int32_t *launches, float *total_ms, int64_t *relaxations)
+                         int32_t *launches, float *total_ms, int64_t *relaxations, int64_t *bytes)
 {
     if (!c) return RK_E_INVAL;
     if (n_kinds) *n_kinds = rk::KFILL_NKINDS;
@@ -465,6 +465,7 @@ int rk_fill_kernel_stats(rk_chain *c, int32_t kind, int32_t *n_kinds, const char
     if (launches) *launches = cnt;
     if (total_ms) *total_ms = sum;
     if (relaxations) *relaxations = c->prof.work[kind];
+    if (bytes) *bytes = c->prof.bytes[kind];
     return RK_OK;
 }
 

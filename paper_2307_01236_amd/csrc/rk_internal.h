@@ -96,6 +96,7 @@ struct Profiler {
     std::vector<int32_t> kinds;      // kernel kind of each bracketed launch
     int32_t n = 0;                   // launches bracketed in the current solve
     int64_t work[8] = {};            // relaxations per kernel kind in the current solve
+    int64_t bytes[8] = {};           // compulsory table traffic per kernel kind
     hipError_t before(int32_t kind);
     hipError_t after();
     void reset(hipStream_t s)
@@ -104,6 +105,7 @@ struct Profiler {
         n = 0;
         kinds.clear();
         for (int64_t &w : work) w = 0;
+        for (int64_t &b : bytes) b = 0;
     }
 };
 

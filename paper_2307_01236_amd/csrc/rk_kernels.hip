@@ -85,9 +85,10 @@ __device__ inline uint32_t xcd_tile(uint32_t g, uint32_t G)
 // the splits i whose two operands are older than the band (both s..i-1 and i..t shorter
 // than tau).  That is a min-plus product, elementwise in m:
 //     acc(s,t) = min_i ap(s,i) + Opt(i, t, m - x_i).
-// A workgroup owns 64 consecutive budgets (lane = m) and SW = 4 SR consecutive rows s; its
-// wave w keeps, per lane, the SR x T accumulators of rows s0..s0+SR-1 (s0 = S0 + SR w)
-// and ends t = s + tau + k.  Splits are taken CI at a time.  The right operands
+// A workgroup owns 64 consecutive budgets (lane = m) and SW consecutive rows s, in row
+// groups of SR rows; each row group's T ends are split over TH waves, so a wave keeps, per
+// lane, the SR x TW accumulators of rows s0..s0+SR-1 and ends t = s + tau + kh + k (TW = T/TH
+// ends from kh on).  Splits are taken CI at a time.  The right operands
 // Opt(i, t, .) of a chunk, for all NQ ends of the workgroup, are staged in LDS (each
 // global row read once, then used by up to SR waves x rows); each wave reads its own left
 // operands ap(s, i).  The next chunk's operands are loaded into registers while the
@@ -112,14 +113,19 @@ __device__ inline uint32_t buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uin
     return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0);
 }
 
-template <int SR, int T>
+template <int SR, int TW, int TH>
 __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t tau)
 {
-    constexpr int NW = 4, SW = SR * NW, CI = PROD_CI;
+    // TH waves share SR rows, each keeping TW of the T = TW TH ends of those rows
+    constexpr int NW = 4, T = TW * TH, SW = SR * NW / TH, CI = PROD_CI;
+    static_assert(NW % TH == 0, "waves split evenly over the ends");
     constexpr int NQ = (SW + T - 1 + NW - 1) / NW * NW;  // staged ends, padded to the waves
     constexpr int JW = NQ / NW;                           // staged rows per wave and split
     static_assert(CI % 2 == 0, "splits are relaxed in pairs");
-    __shared__ uint32_t qs[CI * NQ * 64];
+    // two staging buffers: chunk c is written to buffer c % 2 while waves that are still
+    // relaxing chunk c - 1 read the other one, so one barrier per chunk suffices
+    constexpr int QB = CI * NQ * 64;
+    __shared__ uint32_t qs[2 * QB];
 
     const int32_t L = ch.L;
     const uint32_t lane = threadIdx.x & 63;
@@ -130,7 +136,8 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
     const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);  // row blocks of a column chunk adjacent
     const int32_t S0 = (int32_t)(tile % n_rb) * SW;
     const uint32_t mchunk = tile / n_rb;
-    const int32_t s0 = S0 + wave * SR;
+    const int32_t rg = wave / TH, kh = (wave % TH) * TW;  // row group, first end offset
+    const int32_t s0 = S0 + rg * SR;
     const int64_t stride = tb.stride;
     const int32_t padl = tb.padl;
     const uint32_t m = mchunk * 64 + lane;
@@ -157,11 +164,11 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
         }
     }
 
-    uint32_t acc[SR][T];
+    uint32_t acc[SR][TW];
 #pragma unroll
     for (int r = 0; r < SR; ++r)
 #pragma unroll
-        for (int k = 0; k < T; ++k) acc[r][k] = DINF;
+        for (int k = 0; k < TW; ++k) acc[r][k] = DINF;
 
     // fetch(ic) issues the loads of chunk ic; their values are first used one chunk later
     uint32_t qv[CI][JW], av[CI][SR];
@@ -204,23 +211,24 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
         return c + CI < anchor ? c + CI : DONE;
     };
 
-    const uint32_t *const qw = qs + wave * SR * 64 + lane;
     fetch(anchor);
-    for (int32_t ic = anchor; ic != DONE;) {
+    for (int32_t ic = anchor, buf = 0; ic != DONE; buf ^= 1) {
         const int32_t inext = next_chunk(ic);
+        uint32_t *const qsb = qs + buf * QB;
+        const uint32_t *const qw = qsb + (rg * SR + kh) * 64 + lane;
         // staged row jj*NW + wave of split ic + ii is final iff jj*NW - ii < qlim
         const int32_t qlim = ic - S0 - wave;
         if (qlim > (JW - 1) * NW) {
 #pragma unroll
             for (int ii = 0; ii < CI; ++ii)
 #pragma unroll
-                for (int jj = 0; jj < JW; ++jj) qs[(ii * NQ + jj * NW + wave) * 64 + lane] = qv[ii][jj];
+                for (int jj = 0; jj < JW; ++jj) qsb[(ii * NQ + jj * NW + wave) * 64 + lane] = qv[ii][jj];
         } else {
 #pragma unroll
             for (int ii = 0; ii < CI; ++ii)
 #pragma unroll
                 for (int jj = 0; jj < JW; ++jj)
-                    qs[(ii * NQ + jj * NW + wave) * 64 + lane] = jj * NW - ii < qlim ? qv[ii][jj] : DINF;
+                    qsb[(ii * NQ + jj * NW + wave) * 64 + lane] = jj * NW - ii < qlim ? qv[ii][jj] : DINF;
         }
         // left operand of row r, split ic + ii is final iff r - ii > alim
         const int32_t alim = ic - s0 - tau - 1;
@@ -244,18 +252,17 @@ __global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t
 #pragma unroll
             for (int r = 0; r < SR; ++r)
 #pragma unroll
-                for (int k = 0; k < T; ++k)
+                for (int k = 0; k < TW; ++k)
                     acc[r][k] = min(min(acc[r][k], sat_add(a[ii][r], qw[(ii * NQ + r + k) * 64])),
                                     sat_add(a[ii + 1][r], qw[((ii + 1) * NQ + r + k) * 64]));
-        __syncthreads();
         ic = inext;
     }
     if (m >= (uint32_t)tb.W) return;
 #pragma unroll
     for (int r = 0; r < SR; ++r)
 #pragma unroll
-        for (int k = 0; k < T; ++k) {
-            const int32_t s = s0 + r, t = s + tau + k;
+        for (int k = 0; k < TW; ++k) {
+            const int32_t s = s0 + r, t = s + tau + kh + k;
             if (s < s_end && t < L) tb.opt[row_of(L, s, t) * stride + padl + m] = (int32_t)acc[r][k];
         }
 }
@@ -606,6 +613,35 @@ static int64_t product_work(int32_t L, int32_t W, int32_t tau, int32_t T, int32_
     return n * W;
 }
 
+// Compulsory table traffic of a product launch: the distinct ap rows (s, s+a) and Opt rows
+// (t-b, t) that some real candidate reads, plus the target rows written (and read back when
+// folding into a stored partial); W int32 per row.  Per row s (per end t) the spans a (b)
+// with a real candidate form one interval, the union over the target spans.
+static int64_t product_bytes(int32_t L, int32_t W, int32_t tau, int32_t T, int32_t alo, int32_t ahi,
+                             int32_t blo, int32_t bhi, bool accumulate)
+{
+    int64_t rows = 0;
+    for (int32_t s = 0; s < L - tau; ++s) {
+        int32_t lo = 0x7fffffff, hi = -1;
+        for (int32_t dd = tau; dd < min(tau + T, L - s); ++dd) {
+            const int32_t a0 = max(alo, dd - bhi), a1 = min(ahi - 1, dd - 1 - blo);
+            if (a0 <= a1) lo = min(lo, a0), hi = max(hi, a1);
+        }
+        if (hi >= lo) rows += hi - lo + 1;
+    }
+    for (int32_t t = tau; t < L; ++t) {
+        int32_t lo = 0x7fffffff, hi = -1;
+        for (int32_t dd = tau; dd < min(tau + T, t + 1); ++dd) {
+            const int32_t b0 = max(blo, dd - ahi), b1 = min(bhi - 1, dd - 1 - alo);
+            if (b0 <= b1) lo = min(lo, b0), hi = max(hi, b1);
+        }
+        if (hi >= lo) rows += hi - lo + 1;
+    }
+    int64_t cells = 0;
+    for (int32_t dd = tau; dd < min(tau + T, L); ++dd) cells += L - dd;
+    return (rows + cells * (accumulate ? 2 : 1)) * W * 4;
+}
+
 template <int WD>
 static hipError_t launch_mid(const DevChain &ch, const Tables &tb, hipStream_t stream, int32_t d,
                              int32_t *n, Profiler *prof)
@@ -629,6 +665,9 @@ static hipError_t launch_mid(const DevChain &ch, const Tables &tb, hipStream_t s
     prof->work[KFILL_MID] += lo == 0 ? product_work(ch.L, tb.W, d, WD, 0, WD, 0, WD)
                                      : product_work(ch.L, tb.W, d, WD, lo, d, 0, d) +
                                            product_work(ch.L, tb.W, d, WD, 0, lo, lo, d);
+    prof->bytes[KFILL_MID] += lo == 0 ? product_bytes(ch.L, tb.W, d, WD, 0, WD, 0, WD, false)
+                                      : product_bytes(ch.L, tb.W, d, WD, lo, d, 0, d, true) +
+                                            product_bytes(ch.L, tb.W, d, WD, 0, lo, lo, d, true);
     return hipSuccess;
 }
 
@@ -649,14 +688,15 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
     const int32_t fin_x = (max(tb.W, tb.padl) + FC - 1) / FC;
     for (int32_t d = 0; d < ch.L; ++d) {
         if (d > 0 && d % BAND == 0) {
-            constexpr int SR = 2, SW = 4 * SR;
+            constexpr int SW = 8;  // rows of a product workgroup
             const dim3 grid(((tb.W + 63) / 64) * ((ch.L - d + SW - 1) / SW));
             if ((e = prof->before(KFILL_PRODUCT)) != hipSuccess) return e;
-            hipLaunchKernelGGL((k_product<SR, BAND>), grid, dim3(256), 0, stream, ch, tb, d);
+            hipLaunchKernelGGL((k_product<4, 16, 2>), grid, dim3(256), 0, stream, ch, tb, d);
             if ((e = hipGetLastError()) != hipSuccess) return e;
             if ((e = prof->after()) != hipSuccess) return e;
             ++n;
             prof->work[KFILL_PRODUCT] += product_work(ch.L, tb.W, d, BAND, 0, d, 0, d);
+            prof->bytes[KFILL_PRODUCT] += product_bytes(ch.L, tb.W, d, BAND, 0, d, 0, d, false);
         } else if (d % 16 == 0 && d > 0) {
             if ((e = launch_mid<16>(ch, tb, stream, d, &n, prof)) != hipSuccess) return e;
         } else if (d % 8 == 0 && d > 0) {
@@ -667,8 +707,12 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if ((e = prof->after()) != hipSuccess) return e;
         ++n;
-        const int32_t D = (d / MIDMIN) * MIDMIN;
-        prof->work[KFILL_FINALIZE] += (int64_t)(ch.L - d) * ((D > 0 ? 2 * (d - D) : d) + ch.K) * tb.W;
+        const int32_t D = (d / MIDMIN) * MIDMIN, near = D > 0 ? 2 * (d - D) : d;
+        prof->work[KFILL_FINALIZE] += (int64_t)(ch.L - d) * (near + ch.K) * tb.W;
+        // per cell: two operand rows per split, the stored partial, the case-1 row, the Opt
+        // row written; the ap row written where a later split uses it
+        prof->bytes[KFILL_FINALIZE] +=
+            ((int64_t)(ch.L - d) * (2 * near + (D > 0) + (d > 0) + 1) + (ch.L - d - 1)) * tb.W * 4;
     }
     *launches = n;
     return hipSuccess;

@@ -210,6 +210,10 @@ def test_profiling_counts_launches():
         assert sum(v[1] for v in stats.values()) <= ms * 1.05 + 0.05
         # the kernels' relaxation counts add up to the recurrence's candidate count
         assert sum(v[2] for v in stats.values()) == relaxations(ch.L, ch.K, ch.M)
+        # every fill kernel that runs moves table rows; each row is W int32
+        W = ch.M + 1
+        for name, v in stats.items():
+            assert v[3] % (4 * W) == 0 and (v[3] > 0) == (v[0] > 0 and name != "k_init_inf_rows"), (name, v)
     finally:
         s.close()
 
