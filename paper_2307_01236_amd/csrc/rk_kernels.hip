@@ -778,6 +778,7 @@ hipError_t launch_arg_row(const DevChain &ch, const Tables &tb, int32_t s, int32
 // the lanes share only the choice search at each visited cell.
 // ---------------------------------------------------------------------------------------
 struct Frame { int32_t type, a, b, c; };  // type 0: Build(s=a, t=b, m=c); 1: emit (kind=a, block=b, option=c)
+static_assert(sizeof(Frame) == 4 * sizeof(int32_t), "frames are four int32 in LDS");
 
 __device__ inline uint64_t wave_min_u64(uint64_t v)
 {
@@ -785,13 +786,32 @@ __device__ inline uint64_t wave_min_u64(uint64_t v)
     return v;
 }
 
+// Per visited cell, the lanes evaluate its candidates in parallel with one round of
+// independent loads: a split's left operand comes from ap (which already holds P, the
+// sweep's validity and the saturation), its right operand from Opt at the shifted column;
+// an option's rest from Opt.  The activation sizes (and the options' xbar, when it fits)
+// are copied to LDS first, so no load waits on another.  Shifted columns are clamped into
+// the row's left pad: a candidate whose column would fall left of it is invalid.
+constexpr int32_t BT_XBAR_LDS_MAX = 8192;  // xbar entries kept in LDS (32 KiB)
+
 __global__ __launch_bounds__(64) void k_backtrace(DevChain ch, Tables tb, int32_t m_top,
                                                   rk_op *__restrict__ ops, int64_t cap,
                                                   int64_t *__restrict__ res)
 {
-    extern __shared__ Frame stk[];
+    extern __shared__ int32_t sh[];
     const int32_t lane = threadIdx.x, L = ch.L, K = ch.K;
     const int32_t stack_cap = 2 * L + 8;
+    Frame *const stk = reinterpret_cast<Frame *>(sh);
+    int32_t *const xs = sh + 4 * stack_cap;  // x_0..x_L
+    const bool xbar_lds = (int64_t)L * K <= BT_XBAR_LDS_MAX;
+    int32_t *const xbs = xs + (L + 1);
+    for (int32_t j = lane; j <= L; j += 64) xs[j] = ch.x[j];
+    if (xbar_lds)
+        for (int32_t j = lane; j < L * K; j += 64) xbs[j] = ch.xbar[j];
+    __syncthreads();
+    const int32_t *const c1 = ch.c1, *const need1 = ch.need1, *const xbar = xbar_lds ? xbs : ch.xbar;
+    const int64_t stride = tb.stride;
+    const int32_t padl = tb.padl;
     int32_t sp = 0;
     int64_t n = 0, nfwd = -1, status = 0;
 
@@ -801,26 +821,42 @@ __global__ __launch_bounds__(64) void k_backtrace(DevChain ch, Tables tb, int32_
         ++n;
     };
     auto push = [&](Frame f) { stk[sp] = f; ++sp; };
+    // the key of candidate j of cell (s, t, m): splits i = s+1+j for j < d, then options
+    auto cand = [&](int32_t s, int32_t t, int32_t m, int32_t j) -> uint64_t {
+        const int32_t d = t - s;
+        if (j < d) {
+            const int32_t i = s + 1 + j;
+            const int32_t a = tb.ap[(row_of(L, s, s) + j) * stride + padl + m];
+            const int32_t q = tb.opt[row_of(L, i, t) * stride + padl + m - min(xs[i], padl)];
+            const int64_t v = (int64_t)a + q;
+            return a >= DINF || q >= DINF || v >= DINF ? ~0ull : ((uint64_t)v << 32) | (uint32_t)i;
+        }
+        const int32_t o = j - d, ko = s * K + o;
+        const int32_t rest = t > s ? tb.opt[row_of(L, s + 1, t) * stride + padl + max(m - xbar[ko], -padl)] : 0;
+        const int64_t v = (int64_t)c1[ko] + rest;
+        return m < need1[ko] || rest >= DINF || v >= DINF ? ~0ull : ((uint64_t)v << 32) | (uint32_t)(L + o);
+    };
 
     push(Frame{0, 0, L - 1, m_top});
     while (sp > 0) {
         const Frame f = stk[--sp];
         if (f.type == 1) { emit(f.a, f.b, f.c); continue; }
-        const int32_t s = f.a, t = f.b, m = f.c, d = t - s;
+        const int32_t s = f.a, t = f.b, m = f.c, n_c = t - s + K;
+        const int32_t own = tb.opt[row_of(L, s, t) * stride + padl + m];
         uint64_t key = ~0ull;
-        for (int32_t j = lane; j < d + K; j += 64)
-            key = min(key, j < d ? split_key(ch, tb, s, t, m, s + 1 + j)
-                                 : option_key(ch, tb, s, t, m, j - d));
+        int32_t j = lane;
+        for (; j + 64 < n_c; j += 128) key = min(key, min(cand(s, t, m, j), cand(s, t, m, j + 64)));
+        if (j < n_c) key = min(key, cand(s, t, m, j));
         key = wave_min_u64(key);
         if (key == ~0ull) { status = 1; break; }
-        if ((int32_t)(key >> 32) != opt_at(tb, L, s, t, m)) { status = 2; break; }
+        if ((int32_t)(key >> 32) != own) { status = 2; break; }
         if (sp + 3 > stack_cap) { status = 3; break; }
         const int32_t code = (int32_t)(key & 0xffffffffu);
         if (code >= L) {
             const int32_t o = code - L;
             emit(RK_FWD_SAVE, s, o);
             push(Frame{1, RK_BWD, s, o});
-            if (t > s) push(Frame{0, s + 1, t, m - ch.xbar[s * K + o]});
+            if (t > s) push(Frame{0, s + 1, t, m - xbar[s * K + o]});
         } else {
             const int32_t i = code;
             emit(RK_FWD_NOSAVE, s, -1);
@@ -830,7 +866,7 @@ __global__ __launch_bounds__(64) void k_backtrace(DevChain ch, Tables tb, int32_
             }
             push(Frame{0, s, i - 1, m});
             push(Frame{1, RK_FREE_X, i, -1});
-            push(Frame{0, i, t, m - ch.x[i]});
+            push(Frame{0, i, t, m - xs[i]});
         }
     }
     if (lane == 0) {
@@ -843,7 +879,9 @@ __global__ __launch_bounds__(64) void k_backtrace(DevChain ch, Tables tb, int32_
 hipError_t launch_backtrace(const DevChain &ch, const Tables &tb, int32_t m_top, rk_op *ops,
                             int64_t cap, int64_t *res, hipStream_t stream)
 {
-    const size_t lds = sizeof(Frame) * (size_t)(2 * ch.L + 8);
+    const bool xbar_lds = (int64_t)ch.L * ch.K <= BT_XBAR_LDS_MAX;
+    const size_t lds = sizeof(Frame) * (size_t)(2 * ch.L + 8) + sizeof(int32_t) * (size_t)(ch.L + 1) +
+                       (xbar_lds ? sizeof(int32_t) * (size_t)ch.L * ch.K : 0);
     hipLaunchKernelGGL(k_backtrace, dim3(1), dim3(64), lds, stream, ch, tb, m_top, ops, cap, res);
     return hipGetLastError();
 }
