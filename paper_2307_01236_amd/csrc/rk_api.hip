@@ -45,6 +45,9 @@ struct rk_chain {
 
     rk_op *d_ops = nullptr;  // backtrace output
     int64_t d_ops_cap = 0;
+    int64_t fills = 0;           // solves queued so far
+    int64_t bt_fill = -1;        // the solve whose schedule d_ops holds
+    int64_t bt_res[3] = {0, 0, 0};
     int64_t *d_res = nullptr;
     int16_t *d_argrow = nullptr;
     int32_t d_argrow_cap = 0;
@@ -193,6 +196,7 @@ int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t
     }
     HIPCHK(hipEventRecord(c->ev_fill1, stream));
     c->queued = true;
+    ++c->fills;
     return RK_OK;
 }
 
@@ -379,14 +383,20 @@ int rk_extract_schedule(rk_chain *c, rk_op *ops, int64_t cap, int64_t *n_ops, in
         if (c->d_ops) HIPCHK(hipFree(c->d_ops));
         c->d_ops = nullptr;
         c->d_ops_cap = 0;
+        c->bt_fill = -1;
         if (hipMalloc(&c->d_ops, max_ops * sizeof(rk_op)) != hipSuccess) return RK_E_NOMEM;
         c->d_ops_cap = max_ops;
     }
-    HIPCHK(rk::launch_backtrace(c->dc, c->tb, c->M - c->x[0], c->d_ops, c->d_ops_cap, c->d_res,
-                                c->stream));
-    int64_t res[3] = {0, 0, 0};
-    HIPCHK(hipMemcpyAsync(res, c->d_res, sizeof(res), hipMemcpyDeviceToHost, c->stream));
-    HIPCHK(hipStreamSynchronize(c->stream));
+    // the schedule of this solve is computed once (the two-call protocol asks twice)
+    int64_t *const res = c->bt_res;
+    if (c->bt_fill != c->fills) {
+        c->bt_fill = -1;
+        HIPCHK(rk::launch_backtrace(c->dc, c->tb, c->M - c->x[0], c->d_ops, c->d_ops_cap, c->d_res,
+                                    c->stream));
+        HIPCHK(hipMemcpyAsync(res, c->d_res, 3 * sizeof(int64_t), hipMemcpyDeviceToHost, c->stream));
+        HIPCHK(hipStreamSynchronize(c->stream));
+        c->bt_fill = c->fills;
+    }
     if (res[2] != 0 || res[0] > c->d_ops_cap) return RK_E_INTERNAL;
     *n_ops = res[0];
     if (n_fwd) *n_fwd = res[1];
