@@ -441,15 +441,15 @@ __global__ __launch_bounds__(256) void k_mid(DevChain ch, Tables tb, int32_t tau
 // partial minimum the splits they did not cover (max(i-1-s, t-i) >= D, D = d rounded down
 // to a multiple of MIDMIN) and case 1 (Eq. fe), clamps, writes Opt
 // and the row's left operand ap(s, t+1) for the spans that will split after t.
-// A workgroup covers FC = 1024 budgets of one cell: wave w the 256 columns from
-// mbase + 256 w, lane l the four columns l, l + 64, l + 128, l + 192 of those, so every
-// scalar address serves four coalesced loads.  Splits go in batches of FB with all loads
+// A workgroup covers FC = 512 budgets of one cell: wave w the 128 columns from
+// mbase + 128 w, lane l the columns l and l + 64 of those, so every scalar address serves
+// two coalesced loads.  Splits go in batches of FB with all loads
 // of a batch issued before any is used; the row pointers of a split range advance
 // incrementally.  Case 1 reads one row, Opt(s+1, t, .), at K shifts: the workgroup stages
 // the columns it needs in LDS once (when the largest shift is at most HMAX), loading them
 // together with the first splits.
 // ---------------------------------------------------------------------------------------
-constexpr int32_t FC = 1024;
+constexpr int32_t FC = 512;
 
 // load at a byte offset from a wave-uniform base (one scalar base + one 32-bit lane offset)
 __device__ inline int32_t ldb(const int32_t *base, uint32_t byte_off)
@@ -467,7 +467,7 @@ __device__ inline int32_t ldrow(const int32_t *base, uint32_t pitch, uint32_t by
 
 __global__ __launch_bounds__(256) void k_finalize(DevChain ch, Tables tb, int32_t d)
 {
-    constexpr int32_t FB = 8, NC = 4, NST = (HMAX + FC) / 256;
+    constexpr int32_t FB = 8, NC = FC / 256, NST = (HMAX + FC) / 256;
     __shared__ int32_t seg[HMAX + FC];
     const int32_t L = ch.L, K = ch.K, W = tb.W;
     const uint32_t n_mc = (uint32_t)(max(W, tb.padl) + FC - 1) / FC;
@@ -476,7 +476,7 @@ __global__ __launch_bounds__(256) void k_finalize(DevChain ch, Tables tb, int32_
     const int32_t mbase = (int32_t)(tile % n_mc) * FC;
     const int32_t lane = (int32_t)(threadIdx.x & 63);
     const int32_t wave = __builtin_amdgcn_readfirstlane((int32_t)(threadIdx.x >> 6));
-    const int32_t m0 = mbase + 256 * wave;  // the wave's first column
+    const int32_t m0 = mbase + 64 * NC * wave;  // the wave's first column
     const int32_t ml = m0 + lane;           // column c of the lane: ml + 64 c
     const int64_t stride = tb.stride;
     const uint32_t pitch = (uint32_t)stride * 4u;
