@@ -49,7 +49,7 @@ constexpr int32_t MIDMIN = 8;
 
 // Splits per chunk of the band product (its operand offsets span about
 // PROD_CI * L rows from one chunk base, in 32-bit bytes).
-constexpr int32_t PROD_CI = 4;
+constexpr int32_t PROD_CI = 2;
 
 // Rows of slack before row 0 and after the infinity row of each table.
 constexpr int32_t SLACK = 32;
