@@ -296,10 +296,14 @@ __device__ inline void static_for(F &&f)
     }
 }
 
+// rows (group A) or ends (group B) of a mid product tile
+template <int WD>
+constexpr int mid_rows() { return 4; }
+
 template <int WD, bool GA, bool LO0>
 __global__ __launch_bounds__(256) void k_mid(DevChain ch, Tables tb, int32_t tau, int32_t accumulate)
 {
-    constexpr int R = 4, NS = WD + R - 1, NJ = R + WD - 1;
+    constexpr int R = mid_rows<WD>(), NS = WD + R - 1, NJ = R + WD - 1;
     static_assert(WD == 8 || WD == 16, "widths 8 and 16");
     static_assert(GA || !LO0, "lo == 0 is group A only");
     const int32_t L = ch.L, W = tb.W, lo = tau - WD;
@@ -331,47 +335,41 @@ __global__ __launch_bounds__(256) void k_mid(DevChain ch, Tables tb, int32_t tau
     // operand of end t0 + r.  Operand j: group A the right operand of end s0 + tau + j,
     // group B the left operand of row t0 - tau - WD + 1 + j (rows below 0 clamped to 0).
     uint32_t xoff[NJ], roff[R];
-    const int32_t base = blk * R;                // s0 (A) or t0 - tau (B)
-    int32_t i = GA ? base + lo + 1 : base + 1;   // the tile's first split
-    int64_t rq, ra;  // Opt row (i, first end) and ap row (first row, i - 1) of the current split
+    const int32_t base = blk * R;                     // s0 (A) or t0 - tau (B)
+    const int32_t i0 = GA ? base + lo + 1 : base + 1;  // the tile's first split
+    const int32_t sa = GA ? base : max(base - WD + 1, 0);  // first ap row's start
     if (GA) {
 #pragma unroll
         for (int j = 0; j < NJ; ++j) xoff[j] = (uint32_t)j * pitch + col;
 #pragma unroll
         for (int r = 0; r < R; ++r) roff[r] = (uint32_t)rows_between(base, min(base + r, L - 1)) * pitch + col;
-        rq = row_of(L, i, base + tau);
-        ra = row_of(L, base, i - 1);
     } else {
-        const int32_t sb = base - WD + 1, sc0 = max(sb, 0);
+        const int32_t sb = base - WD + 1;
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) xoff[j] = (uint32_t)rows_between(sc0, max(sb + j, 0)) * pitch + col;
+        for (int j = 0; j < NJ; ++j) xoff[j] = (uint32_t)rows_between(sa, max(sb + j, 0)) * pitch + col;
 #pragma unroll
         for (int r = 0; r < R; ++r) roff[r] = (uint32_t)r * pitch + col;
-        rq = row_of(L, i, base + tau);
-        ra = row_of(L, sc0, i - 1);
     }
 
     uint32_t vr[2][R], vj[2][NJ];
-    // split u is real for operand r in [u - WD + 1, u]; operand j is needed in [rlo, rhi + WD - 1]
-    auto load = [&](auto uc) {
-        constexpr int u = decltype(uc)::value, b = u & 1;
+    // Split u (i = i0 + u) is real for operand r in [u - WD + 1, u]; operand j is needed in
+    // [rlo, rhi + WD - 1].  Splits past L - 1 only serve cells past the table (clamped).
+    auto load = [&](auto uc, auto bc) {
+        constexpr int u = decltype(uc)::value, b = decltype(bc)::value;
         constexpr int rlo = u - WD + 1 > 0 ? u - WD + 1 : 0, rhi = u < R - 1 ? u : R - 1;
         constexpr int jhi = LO0 ? (rhi + WD - 1 < u ? rhi + WD - 1 : u) : rhi + WD - 1;
+        const int32_t i = min(i0 + u, L - 1);
         // a shift x_i > padl happens only when padl >= W: the read lands in the left pad
-        const int32_t xs = min(ch.x[min(i, L - 1)], padl);
-        const __amdgpu_buffer_rsrc_t dq = block_rsrc(tb.opt + rq * stride - xs, opt_end);
-        const __amdgpu_buffer_rsrc_t da = block_rsrc(tb.ap + ra * stride, ap_end);
+        const int32_t xs = min(ch.x[i], padl);
+        const __amdgpu_buffer_rsrc_t dq = block_rsrc(tb.opt + row_of(L, i, base + tau) * stride - xs, opt_end);
+        const __amdgpu_buffer_rsrc_t da = block_rsrc(tb.ap + row_of(L, sa, i0 + u - 1) * stride, ap_end);
 #pragma unroll
         for (int r = rlo; r <= rhi; ++r) vr[b][r] = buf_load(GA ? da : dq, roff[r], 0);
 #pragma unroll
         for (int j = rlo; j <= jhi; ++j) vj[b][j] = buf_load(GA ? dq : da, xoff[j], 0);
-        // next split: Opt row (i+1, t) is L-1-i rows after (i, t); ap rows advance by one
-        rq += max(L - 1 - i, 0);
-        ra += 1;
-        ++i;
     };
-    auto relax = [&](auto uc) {
-        constexpr int u = decltype(uc)::value, b = u & 1;
+    auto relax = [&](auto uc, auto bc) {
+        constexpr int u = decltype(uc)::value, b = decltype(bc)::value;
         constexpr int rlo = u - WD + 1 > 0 ? u - WD + 1 : 0, rhi = u < R - 1 ? u : R - 1;
 #pragma unroll
         for (int r = rlo; r <= rhi; ++r)
@@ -385,26 +383,46 @@ __global__ __launch_bounds__(256) void k_mid(DevChain ch, Tables tb, int32_t tau
                 }
             }
     };
-    load(std::integral_constant<int, 0>{});
-    static_for<0, NS>([&](auto uc) {
-        constexpr int u = decltype(uc)::value;
-        if constexpr (u + 1 < NS) load(std::integral_constant<int, u + 1>{});
-        relax(uc);
-        // the accumulators are final for this split here, and nothing moves across: only
-        // one split's operands are held in registers ahead of their use
+    // The splits in the order u = (p + DL) mod NS, p = 0, 1, ...: the waves of a group (G
+    // consecutive tiles, R rows or ends apart) rotate by R (G - 1 - w) so that they all
+    // start at the same split i; their ranges differ by a shift only, so they keep visiting
+    // equal splits together (also after the wrap) and share their operand rows in L2.
+    auto run = [&](auto dc) {
+        constexpr int DL = decltype(dc)::value;
+        load(std::integral_constant<int, DL % NS>{}, std::integral_constant<int, 0>{});
+        static_for<0, NS>([&](auto pc) {
+            constexpr int p = decltype(pc)::value;
+            if constexpr (p + 1 < NS)
+                load(std::integral_constant<int, (p + 1 + DL) % NS>{}, std::integral_constant<int, (p + 1) & 1>{});
+            relax(std::integral_constant<int, (p + DL) % NS>{}, std::integral_constant<int, p & 1>{});
+            // the accumulators are final for this split here, and nothing moves across: only
+            // one split's operands are held in registers ahead of their use
 #pragma unroll
-        for (int r = 0; r < R; ++r) {
-            if constexpr (WD == 16)
-                asm volatile("" ::"v"(acc[r][0]), "v"(acc[r][1]), "v"(acc[r][2]), "v"(acc[r][3]), "v"(acc[r][4]),
-                             "v"(acc[r][5]), "v"(acc[r][6]), "v"(acc[r][7]), "v"(acc[r][8]), "v"(acc[r][9]),
-                             "v"(acc[r][10]), "v"(acc[r][11]), "v"(acc[r][12]), "v"(acc[r][13]), "v"(acc[r][14]),
-                             "v"(acc[r][15]));
-            else
-                asm volatile("" ::"v"(acc[r][0]), "v"(acc[r][1]), "v"(acc[r][2]), "v"(acc[r][3]), "v"(acc[r][4]),
-                             "v"(acc[r][5]), "v"(acc[r][6]), "v"(acc[r][7]));
-        }
-        __builtin_amdgcn_sched_barrier(0);
-    });
+            for (int r = 0; r < R; ++r) {
+                if constexpr (WD == 16)
+                    asm volatile("" ::"v"(acc[r][0]), "v"(acc[r][1]), "v"(acc[r][2]), "v"(acc[r][3]),
+                                 "v"(acc[r][4]), "v"(acc[r][5]), "v"(acc[r][6]), "v"(acc[r][7]), "v"(acc[r][8]),
+                                 "v"(acc[r][9]), "v"(acc[r][10]), "v"(acc[r][11]), "v"(acc[r][12]),
+                                 "v"(acc[r][13]), "v"(acc[r][14]), "v"(acc[r][15]));
+                else
+                    asm volatile("" ::"v"(acc[r][0]), "v"(acc[r][1]), "v"(acc[r][2]), "v"(acc[r][3]),
+                                 "v"(acc[r][4]), "v"(acc[r][5]), "v"(acc[r][6]), "v"(acc[r][7]));
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        });
+    };
+    constexpr int G = WD == 16 ? 4 : 2;  // waves whose split ranges all share a split
+    static_assert(R * (G - 1) < NS, "a group's ranges overlap");
+    const int32_t wg = wave % G;
+    if constexpr (G == 4) {
+        if (wg == 0) run(std::integral_constant<int, 3 * R>{});
+        else if (wg == 1) run(std::integral_constant<int, 2 * R>{});
+        else if (wg == 2) run(std::integral_constant<int, R>{});
+        else run(std::integral_constant<int, 0>{});
+    } else {
+        if (wg == 0) run(std::integral_constant<int, R>{});
+        else run(std::integral_constant<int, 0>{});
+    }
 
     // store (or fold into the stored partial) through one descriptor per row r: group A
     // cell (s0+r, s0+r+tau+k) is k rows after (s0+r, s0+r+tau); group B cell
@@ -648,7 +666,8 @@ static hipError_t launch_mid(const DevChain &ch, const Tables &tb, hipStream_t s
 {
     hipError_t e;
     const int32_t lo = d - WD;
-    const int32_t n_blk = (ch.L - d + 3) / 4, n_mc = (tb.W + 63) / 64;
+    constexpr int R = mid_rows<WD>();
+    const int32_t n_blk = (ch.L - d + R - 1) / R, n_mc = (tb.W + 63) / 64;
     const dim3 grid((n_blk * n_mc + 3) / 4);
     for (int32_t group = 0; group < (lo == 0 ? 1 : 2); ++group) {
         if ((e = prof->before(KFILL_MID)) != hipSuccess) return e;
