@@ -351,6 +351,12 @@ __global__ __launch_bounds__(256) void k_mid(DevChain ch, Tables tb, int32_t tau
         for (int r = 0; r < R; ++r) roff[r] = (uint32_t)r * pitch + col;
     }
 
+    // the shifts of the tile's splits, read once (a shift x_i > padl happens only when
+    // padl >= W: the read lands in the left pad)
+    int32_t xsh[NS];
+#pragma unroll
+    for (int u = 0; u < NS; ++u) xsh[u] = min(ch.x[min(i0 + u, L - 1)], padl);
+
     uint32_t vr[2][R], vj[2][NJ];
     // Split u (i = i0 + u) is real for operand r in [u - WD + 1, u]; operand j is needed in
     // [rlo, rhi + WD - 1].  Splits past L - 1 only serve cells past the table (clamped).
@@ -359,8 +365,7 @@ __global__ __launch_bounds__(256) void k_mid(DevChain ch, Tables tb, int32_t tau
         constexpr int rlo = u - WD + 1 > 0 ? u - WD + 1 : 0, rhi = u < R - 1 ? u : R - 1;
         constexpr int jhi = LO0 ? (rhi + WD - 1 < u ? rhi + WD - 1 : u) : rhi + WD - 1;
         const int32_t i = min(i0 + u, L - 1);
-        // a shift x_i > padl happens only when padl >= W: the read lands in the left pad
-        const int32_t xs = min(ch.x[i], padl);
+        const int32_t xs = xsh[u];
         const __amdgpu_buffer_rsrc_t dq = block_rsrc(tb.opt + row_of(L, i, base + tau) * stride - xs, opt_end);
         const __amdgpu_buffer_rsrc_t da = block_rsrc(tb.ap + row_of(L, sa, i0 + u - 1) * stride, ap_end);
 #pragma unroll
