@@ -113,11 +113,11 @@ __device__ inline uint32_t buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uin
     return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0);
 }
 
-template <int SR, int TW, int TH>
-__global__ __launch_bounds__(256) void k_product(DevChain ch, Tables tb, int32_t tau)
+template <int SR, int TW, int TH, int NW>
+__global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int32_t tau)
 {
     // TH waves share SR rows, each keeping TW of the T = TW TH ends of those rows
-    constexpr int NW = 4, T = TW * TH, SW = SR * NW / TH, CI = PROD_CI;
+    constexpr int T = TW * TH, SW = SR * NW / TH, CI = PROD_CI;
     static_assert(NW % TH == 0, "waves split evenly over the ends");
     constexpr int NQ = (SW + T - 1 + NW - 1) / NW * NW;  // staged ends, padded to the waves
     constexpr int JW = NQ / NW;                           // staged rows per wave and split
@@ -712,10 +712,10 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
     const int32_t fin_x = (max(tb.W, tb.padl) + FC - 1) / FC;
     for (int32_t d = 0; d < ch.L; ++d) {
         if (d > 0 && d % BAND == 0) {
-            constexpr int SW = 8;  // rows of a product workgroup
+            constexpr int SR = 4, TW = 16, TH = 2, NW = 4, SW = SR * NW / TH;  // product tile
             const dim3 grid(((tb.W + 63) / 64) * ((ch.L - d + SW - 1) / SW));
             if ((e = prof->before(KFILL_PRODUCT)) != hipSuccess) return e;
-            hipLaunchKernelGGL((k_product<4, 16, 2>), grid, dim3(256), 0, stream, ch, tb, d);
+            hipLaunchKernelGGL((k_product<SR, TW, TH, NW>), grid, dim3(NW * 64), 0, stream, ch, tb, d);
             if ((e = hipGetLastError()) != hipSuccess) return e;
             if ((e = prof->after()) != hipSuccess) return e;
             ++n;
