@@ -446,11 +446,15 @@ __global__ __launch_bounds__(256) void k_mid(DevChain ch, Tables tb, int32_t tau
                 if (!GA && k > 0) back += L - 1 - (sr - k);
                 if (GA ? tr + k < L : sr - k >= 0) {
                     int32_t *const p = GA ? rb + (int64_t)k * stride : rb - back * stride;
-                    const __amdgpu_buffer_rsrc_t dr =
-                        __builtin_amdgcn_make_buffer_rsrc(p, (short)0, (int)pitch, 0x00020000);
-                    uint32_t v = acc[r][k];
-                    if (accumulate) v = min(v, (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(dr, (int)cst, 0, 0));
-                    __builtin_amdgcn_raw_buffer_store_b32((int)v, dr, (int)cst, 0, 0);
+                    const int32_t v = (int32_t)acc[r][k];
+                    if (accumulate) {  // fold into the stored partial in L2, no read-back
+                        (void)__hip_atomic_fetch_min((int32_t *)((char *)p + cst), v, __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+                    } else {
+                        const __amdgpu_buffer_rsrc_t dr =
+                            __builtin_amdgcn_make_buffer_rsrc(p, (short)0, (int)pitch, 0x00020000);
+                        __builtin_amdgcn_raw_buffer_store_b32(v, dr, (int)cst, 0, 0);
+                    }
                 }
             }
         }
