@@ -276,8 +276,8 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
 // spans lie below lo.  With lo == 0 the launch covers the splits whose two spans are both
 // below WD (group A with the right span bounded too).  These are splits that one finalize
 // launch per diagonal would otherwise read operand by operand.
-// The two groups are separate launches (both write every cell of the spans, the second
-// one taking the minimum with what the first stored).
+// Both groups write every cell of the spans; each folds into the stored partial with an
+// atomic minimum, so they run in one launch in any order.
 // A wave owns R = 4 rows (group A: rows s0 + r, ends s0 + r + tau + k) or R ends (group B:
 // ends t0 + r, rows t0 + r - tau - k), k < WD, and 64 budgets.  The tile's WD + R - 1
 // splits are unrolled; which (split, row) pairs are real depends only on their positions
@@ -301,18 +301,15 @@ template <int WD>
 constexpr int mid_rows() { return 4; }
 
 template <int WD, bool GA, bool LO0>
-__global__ __launch_bounds__(256) void k_mid(DevChain ch, Tables tb, int32_t tau, int32_t accumulate)
+__device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t tau, int32_t accumulate,
+                                int32_t wave, int32_t g)
 {
     constexpr int R = mid_rows<WD>(), NS = WD + R - 1, NJ = R + WD - 1;
     static_assert(WD == 8 || WD == 16, "widths 8 and 16");
     static_assert(GA || !LO0, "lo == 0 is group A only");
     const int32_t L = ch.L, W = tb.W, lo = tau - WD;
     const int32_t lane = (int32_t)(threadIdx.x & 63);
-    const int32_t wave = __builtin_amdgcn_readfirstlane((int32_t)(threadIdx.x >> 6));
     const int32_t n_blk = (L - tau + R - 1) / R;  // row blocks (A), end blocks (B)
-    const int32_t n_mc = (W + 63) / 64;
-    const int32_t g = (int32_t)xcd_tile(blockIdx.x, gridDim.x) * 4 + wave;
-    if (g >= n_blk * n_mc) return;
     const int32_t mc = g / n_blk, blk = g % n_blk;
     const int64_t stride = tb.stride;
     const uint32_t pitch = (uint32_t)stride * 4u;
@@ -462,6 +459,21 @@ __global__ __launch_bounds__(256) void k_mid(DevChain ch, Tables tb, int32_t tau
 }
 
 
+
+// One launch per level: group A tiles first, then group B (both fold into the partials
+// with atomic min, so they need no order); with lo == 0 only group A, which stores.
+template <int WD, bool LO0>
+__global__ __launch_bounds__(256) void k_mid(DevChain ch, Tables tb, int32_t tau, int32_t accumulate)
+{
+    constexpr int R = mid_rows<WD>();
+    const int32_t wave = __builtin_amdgcn_readfirstlane((int32_t)(threadIdx.x >> 6));
+    const int32_t per_group = (ch.L - tau + R - 1) / R * ((tb.W + 63) / 64);
+    const int32_t g = (int32_t)xcd_tile(blockIdx.x, gridDim.x) * 4 + wave;
+    if (g < per_group)
+        mid_tile<WD, true, LO0>(ch, tb, tau, accumulate, wave, g);
+    else if (!LO0 && g < 2 * per_group)
+        mid_tile<WD, false, false>(ch, tb, tau, accumulate, wave, g - per_group);
+}
 
 // ---------------------------------------------------------------------------------------
 // Finalize one span-length diagonal d: cell (s, s+d), budgets m.  Adds to the products'
@@ -677,19 +689,15 @@ static hipError_t launch_mid(const DevChain &ch, const Tables &tb, hipStream_t s
     const int32_t lo = d - WD;
     constexpr int R = mid_rows<WD>();
     const int32_t n_blk = (ch.L - d + R - 1) / R, n_mc = (tb.W + 63) / 64;
-    const dim3 grid((n_blk * n_mc + 3) / 4);
-    for (int32_t group = 0; group < (lo == 0 ? 1 : 2); ++group) {
-        if ((e = prof->before(KFILL_MID)) != hipSuccess) return e;
-        if (lo == 0)
-            hipLaunchKernelGGL((k_mid<WD, true, true>), grid, dim3(256), 0, stream, ch, tb, d, 0);
-        else if (group == 0)
-            hipLaunchKernelGGL((k_mid<WD, true, false>), grid, dim3(256), 0, stream, ch, tb, d, 1);
-        else
-            hipLaunchKernelGGL((k_mid<WD, false, false>), grid, dim3(256), 0, stream, ch, tb, d, 1);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        if ((e = prof->after()) != hipSuccess) return e;
-        ++*n;
-    }
+    const dim3 grid(((lo == 0 ? 1 : 2) * n_blk * n_mc + 3) / 4);
+    if ((e = prof->before(KFILL_MID)) != hipSuccess) return e;
+    if (lo == 0)
+        hipLaunchKernelGGL((k_mid<WD, true>), grid, dim3(256), 0, stream, ch, tb, d, 0);
+    else
+        hipLaunchKernelGGL((k_mid<WD, false>), grid, dim3(256), 0, stream, ch, tb, d, 1);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = prof->after()) != hipSuccess) return e;
+    ++*n;
     prof->work[KFILL_MID] += lo == 0 ? product_work(ch.L, tb.W, d, WD, 0, WD, 0, WD)
                                      : product_work(ch.L, tb.W, d, WD, lo, d, 0, d) +
                                            product_work(ch.L, tb.W, d, WD, 0, lo, lo, d);
