@@ -857,32 +857,59 @@ __global__ __launch_bounds__(64) void k_backtrace(DevChain ch, Tables tb, int32_
         ++n;
     };
     auto push = [&](Frame f) { stk[sp] = f; ++sp; };
-    // the key of candidate j of cell (s, t, m): splits i = s+1+j for j < d, then options
-    auto cand = [&](int32_t s, int32_t t, int32_t m, int32_t j) -> uint64_t {
-        const int32_t d = t - s;
-        if (j < d) {
-            const int32_t i = s + 1 + j;
-            const int32_t a = tb.ap[(row_of(L, s, s) + j) * stride + padl + m];
-            const int32_t q = tb.opt[row_of(L, i, t) * stride + padl + m - min(xs[i], padl)];
-            const int64_t v = (int64_t)a + q;
-            return a >= DINF || q >= DINF || v >= DINF ? ~0ull : ((uint64_t)v << 32) | (uint32_t)i;
+    // The smallest key over the candidates of cell (s, t, m): candidate j is split i = s+1+j
+    // for j < d, then option j - d.  A lane takes candidates lane + 64u; for each it loads two
+    // values from addresses chosen without branches (split: ap and the shifted Opt; option:
+    // r(F)+r(B) and its rest), all of a batch's loads in flight together.
+    constexpr int NB = 8;
+    const int32_t *const inf_ptr = tb.opt + tb.inf_row * stride + padl;
+    auto cell_key = [&](int32_t s, int32_t t, int32_t m) -> uint64_t {
+        const int32_t d = t - s, n_c = d + K;
+        const int64_t rs = row_of(L, s, s), rest_row = row_of(L, min(s + 1, t), t);
+        uint64_t key = ~0ull;
+        for (int32_t j0 = 0; j0 < n_c; j0 += 64 * NB) {
+            int32_t av[NB], qv[NB], nv[NB];
+#pragma unroll
+            for (int u = 0; u < NB; ++u) {
+                const int32_t j = j0 + lane + 64 * u;
+                const bool split = j < d;
+                const int32_t jc = max(min(j, d - 1), 0), i = s + 1 + jc;  // clamped: addresses only
+                const int32_t ko = s * K + max(min(j - d, K - 1), 0);
+                const int32_t *const pa = split ? tb.ap + (rs + jc) * stride + padl + m : ch.c1 + ko;
+                const int32_t *const pq =
+                    split    ? tb.opt + row_of(L, min(i, L - 1), t) * stride + padl + m - min(xs[i], padl)
+                    : t > s ? tb.opt + rest_row * stride + padl + max(m - xbar[ko], -padl)
+                             : inf_ptr;
+                av[u] = *pa;
+                qv[u] = *pq;
+                nv[u] = ch.need1[ko];
+            }
+#pragma unroll
+            for (int u = 0; u < NB; ++u) {
+                const int32_t j = j0 + lane + 64 * u;
+                if (j >= n_c) continue;
+                if (j < d) {
+                    const int64_t v = (int64_t)av[u] + qv[u];
+                    if (av[u] < DINF && qv[u] < DINF && v < DINF)
+                        key = min(key, ((uint64_t)v << 32) | (uint32_t)(s + 1 + j));
+                } else {
+                    const int32_t rest = t > s ? qv[u] : 0;
+                    const int64_t v = (int64_t)av[u] + rest;
+                    if (m >= nv[u] && rest < DINF && v < DINF)
+                        key = min(key, ((uint64_t)v << 32) | (uint32_t)(L + j - d));
+                }
+            }
         }
-        const int32_t o = j - d, ko = s * K + o;
-        const int32_t rest = t > s ? tb.opt[row_of(L, s + 1, t) * stride + padl + max(m - xbar[ko], -padl)] : 0;
-        const int64_t v = (int64_t)c1[ko] + rest;
-        return m < need1[ko] || rest >= DINF || v >= DINF ? ~0ull : ((uint64_t)v << 32) | (uint32_t)(L + o);
+        return key;
     };
 
     push(Frame{0, 0, L - 1, m_top});
     while (sp > 0) {
         const Frame f = stk[--sp];
         if (f.type == 1) { emit(f.a, f.b, f.c); continue; }
-        const int32_t s = f.a, t = f.b, m = f.c, n_c = t - s + K;
+        const int32_t s = f.a, t = f.b, m = f.c;
         const int32_t own = tb.opt[row_of(L, s, t) * stride + padl + m];
-        uint64_t key = ~0ull;
-        int32_t j = lane;
-        for (; j + 64 < n_c; j += 128) key = min(key, min(cand(s, t, m, j), cand(s, t, m, j + 64)));
-        if (j < n_c) key = min(key, cand(s, t, m, j));
+        uint64_t key = cell_key(s, t, m);
         key = wave_min_u64(key);
         if (key == ~0ull) { status = 1; break; }
         if ((int32_t)(key >> 32) != own) { status = 2; break; }
