@@ -95,6 +95,20 @@ def test_create_rejects_time_overflow():
     assert _create_rc(ch.L, ch.K, *a) == rk.RK_E_OVERFLOW
 
 
+def test_workspace_guard_for_32bit_offsets():
+    # the band product addresses a chunk's operand rows with 32-bit byte offsets: a chain and
+    # budget whose 2L + 64 rows span 4 GiB or more are refused rather than miscomputed
+    ch = make_random_chain(3, 200, 2)
+    h = rk.rk_chain_create(*_args(ch))
+    try:
+        with pytest.raises(rk.RKError) as e:
+            rk.rk_workspace_bytes(h, 3_000_000)  # tables of 0.4 TB would be fine, the offsets not
+        assert e.value.code == rk.RK_E_NOMEM
+        assert rk.rk_workspace_bytes(h, 1000) > 0
+    finally:
+        rk.rk_chain_destroy(h)
+
+
 def test_workspace_bytes():
     ch = make_config_chain(4)
     h = rk.rk_chain_create(*_args(ch))

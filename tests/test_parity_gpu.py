@@ -93,6 +93,19 @@ def test_fuzz_full_tables(idx):
     full_parity(ch, M)
 
 
+@pytest.mark.parametrize("idx", range(4))
+def test_longer_random_chains_full_tables(idx):
+    """Random (not uniform) chains long enough for band products at spans 32, 64 and 96 and
+    for both mid-product levels, including the folds into stored partials (lo > 0)."""
+    rng = np.random.default_rng(777 + idx)
+    L = int(rng.integers(65, 101))
+    K = int(rng.integers(1, 17))
+    ch = make_random_chain(9000 + idx, L, K, xmax=int(rng.integers(1, 40)), amax=int(rng.integers(1, 60)),
+                           tmax=int(rng.integers(0, 20)), tmin=0, small_times=idx % 2 == 1)
+    M = int(rng.integers(store_all_bound(ch) // 4, store_all_bound(ch) + 1))
+    full_parity(ch, min(M, 700))
+
+
 def test_single_block_and_tiny_budgets():
     ch = make_random_chain(77, 1, 4)
     for M in (0, 1, 5, 63, 64, 65, 200):
