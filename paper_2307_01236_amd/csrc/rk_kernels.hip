@@ -62,9 +62,13 @@ __global__ __launch_bounds__(256) void k_init_inf_rows(Tables tb)
 __device__ inline __amdgpu_buffer_rsrc_t block_rsrc(const int32_t *base, const int32_t *end)
 {
     const int64_t bytes = (const char *)end - (const char *)base;
-    const uint32_t n = bytes > 0xffffffffll ? 0xffffffffu : (uint32_t)bytes;
+    const uint32_t n = bytes > 0x7fffffffll ? 0x7fffffffu : (uint32_t)bytes;
     return __builtin_amdgcn_make_buffer_rsrc((void *)base, (short)0, (int)n, 0x00020000);
 }
+
+// A lane offset past every descriptor's range (ranges stay below 2 GiB): a load with it
+// returns 0 without touching memory.
+constexpr uint32_t OOB = 0x80000000u;
 
 
 // ---------------------------------------------------------------------------------------
@@ -177,23 +181,48 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
         // shifted left by min(x_i, padl) columns (a larger x_i reads only the left pad)
         const int32_t *const qb = tb.opt + (row_of(L, ic, t0) - 1) * stride;
         const __amdgpu_buffer_rsrc_t rq = block_rsrc(qb, opt_end);
+        // Operands that are not used are not read: a staged row whose right span
+        // t0 + jj*NW + wave - ic - ii is outside [0, tau), or a left operand whose span
+        // ic + ii - 1 - s0 - r is, loads from OOB (value 0; a candidate it takes part in has
+        // its other operand masked to infinity, or is itself masked when staged).
+        const int32_t qlo = ic - t0 - wave, qhi = ic - S0 - wave;  // kept iff qlo <= jj*NW - ii < qhi
+        const bool qall = qlo <= -(CI - 1) && (JW - 1) * NW < qhi;
         uint32_t rel = 1;
 #pragma unroll
         for (int ii = 0; ii < CI; ++ii) {
             const int32_t i = ic + ii;
             const uint32_t xs = (uint32_t)min(ch.x[min(i, L)], padl);
             const uint32_t so = rel * pitch - 4u * xs;
+            if (qall) {
 #pragma unroll
-            for (int jj = 0; jj < JW; ++jj) qv[ii][jj] = buf_load(rq, qoff[jj], so);
+                for (int jj = 0; jj < JW; ++jj) qv[ii][jj] = buf_load(rq, qoff[jj], so);
+            } else {
+#pragma unroll
+                for (int jj = 0; jj < JW; ++jj) {
+                    const int32_t e = jj * NW - ii;
+                    qv[ii][jj] = buf_load(rq, e >= qlo && e < qhi ? qoff[jj] : OOB, so);
+                }
+            }
             rel += (uint32_t)max(L - 1 - i, 0);
         }
         // left operands: rows (s0 + r, ic + ii - 1), consecutive in ii
         const int32_t *const ab = tb.ap + row_of(L, s0, ic - 1) * stride;
         const __amdgpu_buffer_rsrc_t ra = block_rsrc(ab, ap_end);
+        const int32_t a0 = ic - 1 - s0;
+        if (a0 - (SR - 1) >= 0 && a0 + CI - 1 < tau) {
 #pragma unroll
-        for (int ii = 0; ii < CI; ++ii)
+            for (int ii = 0; ii < CI; ++ii)
 #pragma unroll
-            for (int r = 0; r < SR; ++r) av[ii][r] = buf_load(ra, aoff[r], (uint32_t)ii * pitch);
+                for (int r = 0; r < SR; ++r) av[ii][r] = buf_load(ra, aoff[r], (uint32_t)ii * pitch);
+        } else {
+#pragma unroll
+            for (int ii = 0; ii < CI; ++ii)
+#pragma unroll
+                for (int r = 0; r < SR; ++r) {
+                    const int32_t a = a0 + ii - r;
+                    av[ii][r] = buf_load(ra, a >= 0 && a < tau ? aoff[r] : OOB, (uint32_t)ii * pitch);
+                }
+        }
     };
 
     // Chunk order: neighbouring row blocks share most right operand rows at equal split i,

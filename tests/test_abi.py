@@ -97,7 +97,7 @@ def test_create_rejects_time_overflow():
 
 def test_workspace_guard_for_32bit_offsets():
     # the band product addresses a chunk's operand rows with 32-bit byte offsets: a chain and
-    # budget whose 2L + 64 rows span 4 GiB or more are refused rather than miscomputed
+    # budget whose 2L + 64 rows span 2 GiB or more are refused rather than miscomputed
     ch = make_random_chain(3, 200, 2)
     h = rk.rk_chain_create(*_args(ch))
     try:
