@@ -845,10 +845,18 @@ hipError_t launch_arg_row(const DevChain &ch, const Tables &tb, int32_t s, int32
 struct Frame { int32_t type, a, b, c; };  // type 0: Build(s=a, t=b, m=c); 1: emit (kind=a, block=b, option=c)
 static_assert(sizeof(Frame) == 4 * sizeof(int32_t), "frames are four int32 in LDS");
 
-__device__ inline uint64_t wave_min_u64(uint64_t v)
+// Minimum of a 32-bit value over the 64 lanes of a wavefront (all lanes active): DPP
+// exchanges inside each row of 16 lanes (swap neighbours, swap pairs, rotate by 4 and by 8)
+// leave the row's minimum in every lane; the four row minima are then read as scalars.
+__device__ inline uint32_t wave_min_u32(uint32_t v)
 {
-    for (int off = 32; off > 0; off >>= 1) v = min(v, (uint64_t)__shfl_xor((unsigned long long)v, off, 64));
-    return v;
+    v = min(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xb1, 0xf, 0xf, false));   // quad_perm 1,0,3,2
+    v = min(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4e, 0xf, 0xf, false));   // quad_perm 2,3,0,1
+    v = min(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x124, 0xf, 0xf, false));  // row_ror 4
+    v = min(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x128, 0xf, 0xf, false));  // row_ror 8
+    const uint32_t r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
+    const uint32_t r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
+    return min(min(r0, r1), min(r2, r3));
 }
 
 // Per visited cell, the lanes evaluate its candidates in parallel with one round of
@@ -859,6 +867,7 @@ __device__ inline uint64_t wave_min_u64(uint64_t v)
 // the row's left pad: a candidate whose column would fall left of it is invalid.
 constexpr int32_t BT_XBAR_LDS_MAX = 8192;  // xbar entries kept in LDS (32 KiB)
 
+template <bool XBAR_LDS>
 __global__ __launch_bounds__(64) void k_backtrace(DevChain ch, Tables tb, int32_t m_top,
                                                   rk_op *__restrict__ ops, int64_t cap,
                                                   int64_t *__restrict__ res)
@@ -868,13 +877,12 @@ __global__ __launch_bounds__(64) void k_backtrace(DevChain ch, Tables tb, int32_
     const int32_t stack_cap = 2 * L + 8;
     Frame *const stk = reinterpret_cast<Frame *>(sh);
     int32_t *const xs = sh + 4 * stack_cap;  // x_0..x_L
-    const bool xbar_lds = (int64_t)L * K <= BT_XBAR_LDS_MAX;
     int32_t *const xbs = xs + (L + 1);
     for (int32_t j = lane; j <= L; j += 64) xs[j] = ch.x[j];
-    if (xbar_lds)
+    if (XBAR_LDS)
         for (int32_t j = lane; j < L * K; j += 64) xbs[j] = ch.xbar[j];
     __syncthreads();
-    const int32_t *const c1 = ch.c1, *const need1 = ch.need1, *const xbar = xbar_lds ? xbs : ch.xbar;
+    const int32_t *const xbar = XBAR_LDS ? xbs : ch.xbar;
     const int64_t stride = tb.stride;
     const int32_t padl = tb.padl;
     int32_t sp = 0;
@@ -886,79 +894,86 @@ __global__ __launch_bounds__(64) void k_backtrace(DevChain ch, Tables tb, int32_
         ++n;
     };
     auto push = [&](Frame f) { stk[sp] = f; ++sp; };
-    // The smallest key over the candidates of cell (s, t, m): candidate j is split i = s+1+j
-    // for j < d, then option j - d.  A lane takes candidates lane + 64u; for each it loads two
-    // values from addresses chosen without branches (split: ap and the shifted Opt; option:
-    // r(F)+r(B) and its rest), all of a batch's loads in flight together.
-    constexpr int NB = 8;
-    const int32_t *const inf_ptr = tb.opt + tb.inf_row * stride + padl;
-    auto cell_key = [&](int32_t s, int32_t t, int32_t m) -> uint64_t {
-        const int32_t d = t - s, n_c = d + K;
-        const int64_t rs = row_of(L, s, s), rest_row = row_of(L, min(s + 1, t), t);
-        uint64_t key = ~0ull;
-        for (int32_t j0 = 0; j0 < n_c; j0 += 64 * NB) {
-            int32_t av[NB], qv[NB], nv[NB];
-#pragma unroll
-            for (int u = 0; u < NB; ++u) {
-                const int32_t j = j0 + lane + 64 * u;
-                const bool split = j < d;
-                const int32_t jc = max(min(j, d - 1), 0), i = s + 1 + jc;  // clamped: addresses only
-                const int32_t ko = s * K + max(min(j - d, K - 1), 0);
-                const int32_t *const pa = split ? tb.ap + (rs + jc) * stride + padl + m : ch.c1 + ko;
-                const int32_t *const pq =
-                    split    ? tb.opt + row_of(L, min(i, L - 1), t) * stride + padl + m - min(xs[i], padl)
-                    : t > s ? tb.opt + rest_row * stride + padl + max(m - xbar[ko], -padl)
-                             : inf_ptr;
-                av[u] = *pa;
-                qv[u] = *pq;
-                nv[u] = ch.need1[ko];
-            }
-#pragma unroll
-            for (int u = 0; u < NB; ++u) {
-                const int32_t j = j0 + lane + 64 * u;
-                if (j >= n_c) continue;
-                if (j < d) {
-                    const int64_t v = (int64_t)av[u] + qv[u];
-                    if (av[u] < DINF && qv[u] < DINF && v < DINF)
-                        key = min(key, ((uint64_t)v << 32) | (uint32_t)(s + 1 + j));
-                } else {
-                    const int32_t rest = t > s ? qv[u] : 0;
-                    const int64_t v = (int64_t)av[u] + rest;
-                    if (m >= nv[u] && rest < DINF && v < DINF)
-                        key = min(key, ((uint64_t)v << 32) | (uint32_t)(L + j - d));
-                }
-            }
-        }
-        return key;
-    };
 
-    push(Frame{0, 0, L - 1, m_top});
-    while (sp > 0) {
-        const Frame f = stk[--sp];
-        if (f.type == 1) { emit(f.a, f.b, f.c); continue; }
-        const int32_t s = f.a, t = f.b, m = f.c;
+    // The cell being resolved stays in registers; the stack holds what comes after it.
+    int32_t s = 0, t = L - 1, m = m_top;
+    bool have = true;
+    constexpr int NB = 8;  // split candidates per lane per round of loads
+    for (;;) {
+        if (!have) {
+            if (sp == 0) break;
+            const Frame f = stk[--sp];
+            if (f.type == 1) { emit(f.a, f.b, f.c); continue; }
+            s = f.a; t = f.b; m = f.c;
+        }
+        const int32_t d = t - s;
         const int32_t own = tb.opt[row_of(L, s, t) * stride + padl + m];
-        uint64_t key = cell_key(s, t, m);
-        key = wave_min_u64(key);
-        if (key == ~0ull) { status = 1; break; }
-        if ((int32_t)(key >> 32) != own) { status = 2; break; }
-        if (sp + 3 > stack_cap) { status = 3; break; }
-        const int32_t code = (int32_t)(key & 0xffffffffu);
-        if (code >= L) {
-            const int32_t o = code - L;
+        // This lane's smallest (cost, code) key over its candidates: split i = s+1+j (j < d)
+        // has code i, option o has code L+o.  Addresses of candidates past the end are
+        // clamped into the tables; their values are then ignored.  Row numbers fit 32 bits
+        // (L <= 2000), so each address is one 32x32+64 multiply-add from the table base.
+        uint64_t best = ~0ull;
+        auto take = [&](bool ok, uint32_t v, uint32_t code) {
+            best = min(best, ok ? ((uint64_t)v << 32) | code : ~0ull);
+        };
+        auto row32 = [&](int32_t a, int32_t b) { return (uint32_t)(a * L - ((a * (a - 1)) >> 1) + b - a); };
+        const uint32_t ustride = (uint32_t)stride;
+        const int32_t *const ap_s = tb.ap + (uint64_t)row32(s, s) * ustride + padl + m;
+        const int32_t rest_row = row32(min(s + 1, t), t);
+        const int32_t rounds = max((d + 64 * NB - 1) / (64 * NB), (K + 63) / 64);
+        for (int32_t r = 0; r < rounds; ++r) {
+            // the option's xbar first: when it comes from global memory, the rest's address
+            // waits for it alone, not for the splits' loads
+            const int32_t o = r * 64 + lane, ko = s * K + min(o, K - 1);
+            const int32_t xb = xbar[ko];
+            int32_t xi[NB], av[NB], qv[NB];
+#pragma unroll
+            for (int u = 0; u < NB; ++u) xi[u] = xs[min(s + 1 + r * 64 * NB + 64 * u + lane, t)];
+#pragma unroll
+            for (int u = 0; u < NB; ++u) {
+                const int32_t jc = min(r * 64 * NB + 64 * u + lane, max(d - 1, 0));
+                const int32_t i = min(s + 1 + jc, t);
+                av[u] = ap_s[(uint64_t)(uint32_t)jc * ustride];
+                qv[u] = tb.opt[(uint64_t)row32(i, t) * ustride + (uint32_t)(padl + m - min(xi[u], padl))];
+            }
+            const int32_t c1 = ch.c1[ko], need = ch.need1[ko];
+            const int32_t rest_v = tb.opt[(uint64_t)rest_row * ustride + (uint32_t)(padl + max(m - xb, -padl))];
+            const int32_t rest = t > s ? rest_v : 0;  // row (s, s) stands in when t == s
+#pragma unroll
+            for (int u = 0; u < NB; ++u) {
+                const int32_t j = r * 64 * NB + 64 * u + lane;
+                take(j < d, (uint32_t)av[u] + (uint32_t)qv[u], (uint32_t)(s + 1 + j));
+            }
+            take(o < K && m >= need, (uint32_t)c1 + (uint32_t)rest, (uint32_t)(L + o));
+        }
+        const uint32_t bc = (uint32_t)(best >> 32), bk = (uint32_t)best;
+        const uint32_t cost = wave_min_u32(bc);
+        const uint32_t code = wave_min_u32(bc == cost ? bk : ~0u);
+        if (cost >= (uint32_t)DINF) { status = 1; break; }
+        if ((int32_t)cost != own) { status = 2; break; }
+        if (sp + 2 > stack_cap) { status = 3; break; }
+        if (code >= (uint32_t)L) {
+            const int32_t o = (int32_t)code - L;
             emit(RK_FWD_SAVE, s, o);
             push(Frame{1, RK_BWD, s, o});
-            if (t > s) push(Frame{0, s + 1, t, m - xbar[s * K + o]});
+            have = t > s;
+            m -= xbar[s * K + o];
+            s += 1;
         } else {
-            const int32_t i = code;
+            // forward through blocks s..i-1 keeping nothing, dropping x_{s+1}..x_{i-1} behind
+            const int32_t i = (int32_t)code;
             emit(RK_FWD_NOSAVE, s, -1);
-            for (int32_t k = s + 1; k < i; ++k) {
-                emit(RK_FWD_NOSAVE, k, -1);
-                emit(RK_FREE_X, k, -1);
+            for (int32_t k = lane; k < i - s - 1; k += 64) {
+                const int64_t at = n + 2 * (int64_t)k;
+                if (at < cap) ops[at] = rk_op{RK_FWD_NOSAVE, s + 1 + k, -1};
+                if (at + 1 < cap) ops[at + 1] = rk_op{RK_FREE_X, s + 1 + k, -1};
             }
+            n += 2 * (int64_t)(i - s - 1);
             push(Frame{0, s, i - 1, m});
             push(Frame{1, RK_FREE_X, i, -1});
-            push(Frame{0, i, t, m - xs[i]});
+            have = true;
+            s = i;
+            m -= xs[i];
         }
     }
     if (lane == 0) {
@@ -974,7 +989,10 @@ hipError_t launch_backtrace(const DevChain &ch, const Tables &tb, int32_t m_top,
     const bool xbar_lds = (int64_t)ch.L * ch.K <= BT_XBAR_LDS_MAX;
     const size_t lds = sizeof(Frame) * (size_t)(2 * ch.L + 8) + sizeof(int32_t) * (size_t)(ch.L + 1) +
                        (xbar_lds ? sizeof(int32_t) * (size_t)ch.L * ch.K : 0);
-    hipLaunchKernelGGL(k_backtrace, dim3(1), dim3(64), lds, stream, ch, tb, m_top, ops, cap, res);
+    if (xbar_lds)
+        hipLaunchKernelGGL(k_backtrace<true>, dim3(1), dim3(64), lds, stream, ch, tb, m_top, ops, cap, res);
+    else
+        hipLaunchKernelGGL(k_backtrace<false>, dim3(1), dim3(64), lds, stream, ch, tb, m_top, ops, cap, res);
     return hipGetLastError();
 }
 
