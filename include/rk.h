@@ -90,8 +90,9 @@ void rk_chain_destroy(rk_chain *c);
 
 /* Bytes of device workspace a solve of this chain at budget M needs (the
  * Opt table and its companions).  RK_E_INVAL for M outside [0, RK_MAX_M];
- * RK_E_NOMEM when 2L + 64 table rows would span 2 GiB or more (the kernels
- * address operand blocks with 32-bit offsets) or the tables exceed 2^40 int32. */
+ * RK_E_NOMEM when 18L + 64 table rows would span 2 GiB or more (the kernels
+ * address operand blocks with 32-bit offsets; at L = 384 this allows budgets up
+ * to about 77 000) or the tables exceed 2^40 int32. */
 int rk_workspace_bytes(const rk_chain *c, int32_t M, size_t *bytes);
 
 /*

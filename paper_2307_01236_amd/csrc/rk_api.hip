@@ -97,7 +97,8 @@ int geometry(const rk_chain *c, int32_t M, Geometry *g, size_t *bytes)
     if (elems <= 0 || elems > (int64_t(1) << 40)) return RK_E_NOMEM;
     // the band product addresses the operand rows of one chunk of splits with 32-bit byte
     // offsets from a chunk base
-    if ((rk::PROD_CI * (int64_t)c->L + 64) * g->stride * 4 >= (int64_t(1) << 31)) return RK_E_NOMEM;
+    if ((rk::OFFSET_SPAN_L * (int64_t)c->L + rk::OFFSET_SPAN_C) * g->stride * 4 >= (int64_t(1) << 31))
+        return RK_E_NOMEM;
     *bytes = (size_t)elems * sizeof(int32_t);
     return RK_OK;
 }

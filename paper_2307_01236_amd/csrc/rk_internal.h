@@ -47,9 +47,15 @@ static_assert(RK_TIME_LIMIT < DINF, "finite values must stay below the device in
 constexpr int32_t BAND = 32;
 constexpr int32_t MIDMIN = 8;
 
-// Splits per chunk of the band product (its operand offsets span about
-// PROD_CI * L rows from one chunk base, in 32-bit bytes).
+// Splits per chunk of the band product.
 constexpr int32_t PROD_CI = 2;
+
+// The products address an operand block through one buffer descriptor with 32-bit byte
+// offsets from its first row.  The widest block spans at most OFFSET_SPAN_L * (L - 1) +
+// OFFSET_SPAN_C rows: a width-16 mid tile's group B reads left operands of 18 consecutive
+// rows s, each L - 1 - s rows after the previous one (the band product's blocks span at most
+// 3 (L - 1) + 2 and L + 41 rows).  A workspace whose span reaches 2 GiB is refused.
+constexpr int32_t OFFSET_SPAN_L = 18, OFFSET_SPAN_C = 64;
 
 // Rows of slack before row 0 and after the infinity row of each table.
 constexpr int32_t SLACK = 32;

@@ -123,6 +123,7 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
     // TH waves share SR rows, each keeping TW of the T = TW TH ends of those rows
     constexpr int T = TW * TH, SW = SR * NW / TH, CI = PROD_CI;
     static_assert(NW % TH == 0, "waves split evenly over the ends");
+    static_assert(SR - 1 <= OFFSET_SPAN_L && CI - 1 <= OFFSET_SPAN_L, "operand offsets fit the workspace guard");
     constexpr int NQ = (SW + T - 1 + NW - 1) / NW * NW;  // staged ends, padded to the waves
     constexpr int JW = NQ / NW;                           // staged rows per wave and split
     static_assert(CI % 2 == 0, "splits are relaxed in pairs");
@@ -336,6 +337,7 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
     constexpr int R = mid_rows<WD>(), NS = WD + R - 1, NJ = R + WD - 1;
     static_assert(WD == 8 || WD == 16, "widths 8 and 16");
     static_assert(GA || !LO0, "lo == 0 is group A only");
+    static_assert(NJ - 1 <= OFFSET_SPAN_L && NJ + 1 <= OFFSET_SPAN_C, "operand offsets fit the workspace guard");
     const int32_t L = ch.L, W = tb.W, lo = tau - WD;
     const int32_t lane = (int32_t)(threadIdx.x & 63);
     const int32_t n_blk = (L - tau + R - 1) / R;  // row blocks (A), end blocks (B)

@@ -96,13 +96,22 @@ def test_create_rejects_time_overflow():
 
 
 def test_workspace_guard_for_32bit_offsets():
-    # the band product addresses a chunk's operand rows with 32-bit byte offsets: a chain and
-    # budget whose 2L + 64 rows span 2 GiB or more are refused rather than miscomputed
-    ch = make_random_chain(3, 200, 2)
+    # the products address an operand block with 32-bit byte offsets from its first row; the
+    # widest block (a mid tile's left operands of 18 rows s) spans 18 (L - 1) rows: a chain
+    # and budget whose 18 L + 64 rows span 2 GiB or more are refused rather than miscomputed
+    ch = make_random_chain(3, 384, 2, xmax=7)
     h = rk.rk_chain_create(*_args(ch))
     try:
+        def row_bytes(M):  # a 64-column pad (max x_i <= 7) plus the budget columns, 64-aligned
+            return (64 + (M + 1 + 63) // 64 * 64) * 4
+        span = 18 * ch.L + 64
+        ok = max(M for M in range(70_000, 80_000, 64) if span * row_bytes(M) < 2 ** 31)
+        assert rk.rk_workspace_bytes(h, ok) > 0  # ~60 GB of tables: accepted
         with pytest.raises(rk.RKError) as e:
-            rk.rk_workspace_bytes(h, 3_000_000)  # tables of 0.4 TB would be fine, the offsets not
+            rk.rk_workspace_bytes(h, ok + 64)
+        assert e.value.code == rk.RK_E_NOMEM
+        with pytest.raises(rk.RKError) as e:
+            rk.rk_workspace_bytes(h, 3_000_000)
         assert e.value.code == rk.RK_E_NOMEM
         assert rk.rk_workspace_bytes(h, 1000) > 0
     finally:
