@@ -2,7 +2,8 @@
 
 One step is one pass of the whole hot path over one chain: the table fill for
 every span and every budget (App. C, Alg. 2), the answer read-back, and the
-schedule (Alg. 3) copied to the host.  The chain is the deep transformer-like
+schedule (Alg. 3) copied to the host.  Outside the timed steps it also reports
+the memory/time trade-off curve of the fill against Rotor's (Sec. 4).  The chain is the deep transformer-like
 workload, 384 blocks with 16 options each at a 6000-slot budget, created and
 uploaded before the timed region; the table lives in a torch allocation and
 the solve runs on a torch stream.
@@ -164,6 +165,26 @@ def main():
     s.schedule()
     sched_ms = (time.perf_counter() - t) * 1e3
 
+    # Sec. 4's comparison with Rotor on the same chain: the trade-off curve of this fill (every
+    # budget's optimum) against one of Rotor's choice set (keep everything or nothing per
+    # block: option 0), as overhead over the time with no recomputation
+    t = time.perf_counter()
+    curve = s.tradeoff_curve()
+    curve_ms = (time.perf_counter() - t) * 1e3
+    rot = rk.Solver(ch.options([0]))
+    rot.solve(M)
+    rcurve = rot.tradeoff_curve()
+    rot.close()
+    ideal = int((ch.fwd.astype("int64") + ch.bwd).min(axis=1).sum())
+    budgets = [int(M * f) for f in (0.1, 0.2, 0.3, 0.5, 0.75, 1.0)]
+    ovh = lambda v: None if v == rk.RK_INF else round(int(v) / ideal - 1.0, 4)
+    tradeoff = {"curve_read_ms": curve_ms, "budgets": budgets,
+                "rk_rotor_overhead": [ovh(curve[b]) for b in budgets],
+                "rotor_overhead": [ovh(rcurve[b]) for b in budgets],
+                "min_budget_rk_rotor": int((curve < rk.RK_INF).argmax()),
+                "min_budget_rotor": int((rcurve < rk.RK_INF).argmax())}
+    log(f"trade-off: {tradeoff}")
+
     # dominant kernel: the one with the most device time; both of its roofs per launch
     dname, (dn, dms, dwork, dbytes) = max(kern.items(), key=lambda kv: kv[1][1])
     per_launch_s = dms / dn * 1e-3
@@ -201,7 +222,7 @@ def main():
         "wall_solve_ms": statistics.median(wall), "fill_ms": statistics.median(fill_ms),
         "schedule_ms": sched_ms,
         "fill_relax_per_s": relax / (statistics.median(fill_ms) * 1e-3),
-        "roofline": roofline, "cpu_baseline": cpu,
+        "roofline": roofline, "cpu_baseline": cpu, "tradeoff": tradeoff,
         "kernels": {k: {"launches_per_step": v[0] / args.steps, "ms_per_step": v[1] / args.steps,
                         "relaxations_per_step": v[2] // args.steps, "table_bytes_per_step": v[3] // args.steps}
                     for k, v in kern.items()},

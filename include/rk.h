@@ -141,6 +141,17 @@ int rk_extract_schedule(rk_chain *c, rk_op *ops, int64_t cap, int64_t *n_ops, in
 int rk_read_row(rk_chain *c, int32_t s, int32_t t, int32_t *opt_row, int16_t *arg_row);
 
 /*
+ * The memory/time trade-off of the last solve, the curve of the paper's
+ * comparison with Rotor (Sec. 4, overhead against peak memory): times[b] is the
+ * best schedule time within a total budget of b slots, Opt(0, L-1, b - x_0), or
+ * RK_INF when b < x_0 or no schedule fits, for b = 0 .. n-1.  One fill at budget
+ * M answers every smaller budget (Alg. 2 fills all m <= M), so n may be at most
+ * M + 1 of the last solve.  times is host memory the caller owns.  RK_E_INVAL
+ * for n outside [0, M + 1] or NULL times with n > 0; RK_E_NOT_SOLVED before a solve.
+ */
+int rk_tradeoff_curve(rk_chain *c, int32_t *times, int64_t n);
+
+/*
  * Device time of the last solve's table fill, in milliseconds (HIP events
  * around the fill on the solve's stream), and the number of kernels launched.
  */

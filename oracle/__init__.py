@@ -151,6 +151,21 @@ def solve(ch, M: int | None = None, lib: Library | None = None) -> Solution:
     return Solution(ch, M, opt, arg, int(ans.value))
 
 
+def tradeoff_curve(sol: Solution, n: int | None = None) -> np.ndarray:
+    """Best schedule time at each total budget b = 0..n-1 (default n = M+1): the answer of
+    the solve at budget b, Opt(0, L-1, b - x_0), INF below x_0 (Sec. 4's overhead-against-
+    memory comparison reads this curve).  A fill at M holds every smaller budget's answer,
+    because Opt(s, t, m) does not depend on the largest budget filled."""
+    ch = sol.chain
+    n = sol.M + 1 if n is None else int(n)
+    assert 0 <= n <= sol.M + 1
+    x0 = int(ch.x[0])
+    out = np.full(n, INF, dtype=np.int64)
+    if n > x0:
+        out[x0:] = sol.opt_row(0, ch.L - 1)[: n - x0]
+    return out
+
+
 def schedule(sol: Solution, M: int | None = None, lib: Library | None = None):
     """Alg. 3 for budget M (default: the solve's M).  Returns (ops[n,3], n_fwd) or None."""
     lib = _load(lib)

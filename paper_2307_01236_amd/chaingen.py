@@ -77,6 +77,16 @@ class Chain:
                      tmp_bwd=self.tmp_bwd[s:t + 1].copy(), M=self.M,
                      name=f"{self.name}[{s}:{t}]")
 
+    def options(self, keep) -> "Chain":
+        """The same blocks with only the saving options listed in `keep` (in that order).
+        keep=[0] leaves each block the option that keeps all its intermediates, which is
+        Rotor's choice set (store everything or nothing per block)."""
+        keep = list(keep)
+        pick = lambda a: np.ascontiguousarray(a[:, keep])
+        return Chain(L=self.L, K=len(keep), x=self.x.copy(), fn_time=self.fn_time.copy(),
+                     fn_tmp=self.fn_tmp.copy(), fwd=pick(self.fwd), bwd=pick(self.bwd),
+                     mem=pick(self.mem), tmp_fwd=pick(self.tmp_fwd), tmp_bwd=pick(self.tmp_bwd),
+                     M=self.M, name=f"{self.name}{{options {keep}}}")
 
 # name, L, K, M, block-structure kind
 CONFIGS = [

@@ -434,6 +434,25 @@ int rk_read_row(rk_chain *c, int32_t s, int32_t t, int32_t *opt_row, int16_t *ar
     return RK_OK;
 }
 
+int rk_tradeoff_curve(rk_chain *c, int32_t *times, int64_t n)
+{
+    if (!c || (!times && n > 0) || n < 0) return RK_E_INVAL;
+    if (!c->queued) return RK_E_NOT_SOLVED;
+    if (n > (int64_t)c->W) return RK_E_INVAL;
+    DeviceScope ds(c);
+    if (!ds.ok) return RK_E_DEVICE;
+    HIPCHK(hipEventSynchronize(c->ev_fill1));
+    // budget b leaves b - x_0 slots beyond the chain input: Opt(0, L-1, b - x_0)
+    const int64_t x0 = c->x[0], lead = std::min<int64_t>(n, x0);
+    for (int64_t b = 0; b < lead; ++b) times[b] = RK_INF;
+    if (n > x0) {
+        const int64_t base = rk::row_of(c->L, 0, c->L - 1) * c->tb.stride + c->tb.padl;
+        HIPCHK(hipMemcpy(times + x0, c->tb.opt + base, (size_t)(n - x0) * sizeof(int32_t), hipMemcpyDeviceToHost));
+        for (int64_t b = x0; b < n; ++b) times[b] = to_abi(times[b]);
+    }
+    return RK_OK;
+}
+
 int rk_last_fill_ms(rk_chain *c, float *ms, int32_t *launches)
 {
     if (!c || !ms) return RK_E_INVAL;

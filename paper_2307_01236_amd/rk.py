@@ -23,7 +23,8 @@ RK_FWD_NOSAVE, RK_FWD_SAVE, RK_BWD, RK_FREE_X = 0, 1, 2, 3
  RK_E_BUFSZ, RK_E_INTERNAL) = 0, -1, -2, -3, -4, -5, -6, -7, -8
 
 EXPORTS = ("rk_chain_create", "rk_chain_destroy", "rk_workspace_bytes", "rk_solve", "rk_solve_async",
-           "rk_result", "rk_extract_schedule", "rk_read_row", "rk_last_fill_ms", "rk_set_profiling",
+           "rk_result", "rk_extract_schedule", "rk_read_row", "rk_tradeoff_curve", "rk_last_fill_ms",
+           "rk_set_profiling",
            "rk_fill_kernel_stats", "rk_strerror")
 
 
@@ -62,6 +63,7 @@ def load():
         lib.rk_result.argtypes = [C.c_void_p, i32p]
         lib.rk_extract_schedule.argtypes = [C.c_void_p, P(rk_op), i64, P(i64), P(i64)]
         lib.rk_read_row.argtypes = [C.c_void_p, i32, i32, i32p, P(C.c_int16)]
+        lib.rk_tradeoff_curve.argtypes = [C.c_void_p, i32p, i64]
         lib.rk_last_fill_ms.argtypes = [C.c_void_p, P(C.c_float), i32p]
         lib.rk_set_profiling.argtypes = [C.c_void_p, i32]
         lib.rk_fill_kernel_stats.argtypes = [C.c_void_p, i32, i32p, P(C.c_char_p), i32p,
@@ -149,6 +151,13 @@ def rk_read_row(h, s: int, t: int, W: int, want_arg: bool = True):
     return opt, arg
 
 
+def rk_tradeoff_curve(h, n: int) -> np.ndarray:
+    times = np.empty(max(int(n), 0), dtype=np.int32)
+    _check(load().rk_tradeoff_curve(h, times.ctypes.data_as(C.POINTER(C.c_int32)), int(n)),
+           "rk_tradeoff_curve")
+    return times
+
+
 def rk_last_fill_ms(h):
     ms, n = C.c_float(0), C.c_int32(0)
     _check(load().rk_last_fill_ms(h, C.byref(ms), C.byref(n)), "rk_last_fill_ms")
@@ -202,6 +211,10 @@ class Solver:
 
     def row(self, s: int, t: int, want_arg: bool = True):
         return rk_read_row(self.h, s, t, self.M + 1, want_arg)
+
+    def tradeoff_curve(self, n: int | None = None) -> np.ndarray:
+        """Best schedule time at every total budget 0..n-1 (default: up to the solve's M)."""
+        return rk_tradeoff_curve(self.h, self.M + 1 if n is None else n)
 
     def rows(self, want_arg: bool = True):
         """All rows in upper-triangle row-major order of (s,t): ([ncells, W] opt, arg)."""

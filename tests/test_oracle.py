@@ -207,6 +207,35 @@ def test_store_all_regime():
     check_store_all(random_mid_chains()[:4])
 
 
+# ---- trade-off curve (Sec. 4, comparison with Rotor) ----------------------------------------
+
+def test_tradeoff_curve_is_every_budgets_optimum():
+    """The curve read from one fill at budget M equals, at every total budget b <= M, the
+    cheapest enumerated rk-Rotor-shaped schedule whose replay peaks at or below b (no dynamic
+    program involved), INF where none fits (every b below x_0 included)."""
+    for ch in tiny_chains(12, seed0=200):
+        curve = oracle.tradeoff_curve(oracle.solve(ch))
+        assert np.array_equal(curve, brute.decision_trees(ch, ch.M)), ch.name
+        assert (curve[: int(ch.x[0])] == INF).all()
+        part = oracle.tradeoff_curve(oracle.solve(ch), 7)
+        assert np.array_equal(part, curve[:7])
+
+
+def test_rotor_curve_lies_above():
+    """Rotor's choice set (per block, keep everything or nothing: option 0 here) is a subset of
+    rk-Rotor's, so its curve is on or above rk-Rotor's at every budget; with room for
+    everything both reach their closed-form store-all times, and rk-Rotor's first feasible
+    budget is no larger."""
+    for ch in random_mid_chains()[:5]:
+        big = store_all_bound(ch) * 2
+        rk = oracle.tradeoff_curve(oracle.solve(ch, big))
+        rot = oracle.tradeoff_curve(oracle.solve(ch.options([0]), big))
+        assert (rot >= rk).all(), ch.name
+        c1 = ch.fwd.astype(np.int64) + ch.bwd
+        assert rk[-1] == c1.min(axis=1).sum() and rot[-1] == c1[:, 0].sum()
+        assert np.argmax(rk < INF) <= np.argmax(rot < INF)
+
+
 # ---- schedules --------------------------------------------------------------------------
 
 def check_replay(ch, Ms, lib=None):

@@ -254,3 +254,61 @@ def test_graph_replays_match_oracle():
     finally:
         s.close()
         t.close()
+
+
+def test_tradeoff_curve_matches_oracle():
+    """Sec. 4's overhead-against-memory curve from one fill: every budget's optimum, read from
+    the table's top row, equals the oracle's; re-solving at a smaller budget agrees."""
+    for ch, M in [(make_config_chain(0), None), (make_config_chain(1), None), (make_config_chain(2), None)] + \
+            fuzz_chains()[:6]:
+        M = ch.M if M is None else M
+        sol = oracle.solve(ch, M)
+        s = rk.Solver(ch)
+        try:
+            s.solve(M)
+            curve = s.tradeoff_curve().astype(np.int64)
+            assert np.array_equal(curve, oracle.tradeoff_curve(sol)), ch.name
+            assert np.array_equal(s.tradeoff_curve(min(5, M + 1)), curve[: min(5, M + 1)])
+            b = M // 2
+            if b >= 0:
+                assert s.solve(b) == curve[b]
+        finally:
+            s.close()
+
+
+def test_rotor_against_rk_rotor_curves():
+    """Rotor (one saving option per block, keep everything) against rk-Rotor's K options on
+    the tie-heavy GPT-like workload: the GPU curves equal the oracle's on sampled budgets and
+    rk-Rotor's lies on or below Rotor's everywhere."""
+    ch = make_config_chain(1)
+    rot_ch = ch.options([0])
+    curves = []
+    for c in (ch, rot_ch):
+        s = rk.Solver(c)
+        try:
+            s.solve(c.M)
+            curves.append(s.tradeoff_curve().astype(np.int64))
+        finally:
+            s.close()
+        sol = oracle.solve(c)
+        assert np.array_equal(curves[-1], oracle.tradeoff_curve(sol)), c.name
+    rkc, rot = curves
+    assert (rot >= rkc).all()
+    assert np.argmax(rkc < INF) <= np.argmax(rot < INF)
+
+
+def test_tradeoff_curve_errors():
+    ch = make_config_chain(0)
+    s = rk.Solver(ch)
+    try:
+        with pytest.raises(rk.RKError) as e:
+            s.M = ch.M
+            s.tradeoff_curve()
+        assert e.value.code == rk.RK_E_NOT_SOLVED
+        s.solve(ch.M)
+        with pytest.raises(rk.RKError) as e:
+            s.tradeoff_curve(ch.M + 2)
+        assert e.value.code == rk.RK_E_INVAL
+        assert s.tradeoff_curve(0).size == 0
+    finally:
+        s.close()
