@@ -3,7 +3,8 @@
 One step is one pass of the whole hot path over one chain: the table fill for
 every span and every budget (App. C, Alg. 2), the answer read-back, and the
 schedule (Alg. 3) copied to the host.  Outside the timed steps it also reports
-the memory/time trade-off curve of the fill against Rotor's (Sec. 4).  The chain is the deep transformer-like
+the memory/time trade-off curve of the fill against Rotor's (Sec. 4) and the
+effect of option pruning on a chain with an emulated budget-grid option search.  The chain is the deep transformer-like
 workload, 384 blocks with 16 options each at a 6000-slot budget, created and
 uploaded before the timed region; the table lives in a torch allocation and
 the solve runs on a torch stream.
@@ -185,6 +186,26 @@ def main():
                 "min_budget_rotor": int((rcurve < rk.RK_INF).argmax())}
     log(f"trade-off: {tradeoff}")
 
+    # Option pruning (Sec. 3, Phase 2: the budget grid of the option search repeats options):
+    # an emulated 20 x 20 grid search gives 400 options per block on a 96-block chain; the
+    # fill with the distinct ones only against the fill with all of them
+    from paper_2307_01236_amd.chaingen import make_grid_chain
+    g = make_grid_chain(1, 96)
+    pruning = {"workload": g.name, "L": g.L, "K": g.K, "M": g.M}
+    gs = rk.Solver(g)
+    for on in (True, False):
+        gs.set_option_pruning(on)
+        k_run = gs.options()[1]
+        fills = []
+        for _ in range(4):
+            gs.solve(g.M)
+            fills.append(gs.fill_ms()[0])
+        key = "pruned" if on else "all_options"
+        pruning[key] = {"k_run": k_run, "fill_ms": statistics.median(fills[1:]),
+                        "relaxations": relaxations(g.L, k_run, g.M), "answer": gs.result()}
+    gs.close()
+    log(f"option pruning: {pruning}")
+
     # dominant kernel: the one with the most device time; both of its roofs per launch
     dname, (dn, dms, dwork, dbytes) = max(kern.items(), key=lambda kv: kv[1][1])
     per_launch_s = dms / dn * 1e-3
@@ -222,7 +243,7 @@ def main():
         "wall_solve_ms": statistics.median(wall), "fill_ms": statistics.median(fill_ms),
         "schedule_ms": sched_ms,
         "fill_relax_per_s": relax / (statistics.median(fill_ms) * 1e-3),
-        "roofline": roofline, "cpu_baseline": cpu, "tradeoff": tradeoff,
+        "roofline": roofline, "cpu_baseline": cpu, "tradeoff": tradeoff, "option_pruning": pruning,
         "kernels": {k: {"launches_per_step": v[0] / args.steps, "ms_per_step": v[1] / args.steps,
                         "relaxations_per_step": v[2] // args.steps, "table_bytes_per_step": v[3] // args.steps}
                     for k, v in kern.items()},

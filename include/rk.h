@@ -165,7 +165,8 @@ int rk_last_fill_ms(rk_chain *c, float *ms, int32_t *launches);
  * (0 <= kind < *n_kinds), its name as a profiler shows it, the number of its
  * launches in the last solve, their summed device time in milliseconds, the
  * number of candidate evaluations of the recurrence (relaxations, counting
- * only valid (s,t,m,choice) combinations) those launches performed, and their
+ * only valid (s,t,m,choice) combinations, with k_run option slots per block; see
+ * rk_chain_options) those launches performed, and their
  * compulsory table traffic in bytes: every table row a launch reads counted
  * once, its budget columns only, plus every row it writes (and reads back, where
  * it folds into a stored partial).  Any output pointer may be NULL.  Waits for
@@ -175,6 +176,27 @@ int rk_last_fill_ms(rk_chain *c, float *ms, int32_t *launches);
 int rk_set_profiling(rk_chain *c, int32_t enable);
 int rk_fill_kernel_stats(rk_chain *c, int32_t kind, int32_t *n_kinds, const char **name,
                          int32_t *launches, float *total_ms, int64_t *relaxations, int64_t *bytes);
+
+/*
+ * Options the solver evaluates (Sec. 3, Phase 2: the paper's option search returns many
+ * repeated solutions for the budget grid, and rk-Rotor needs only the distinct ones).
+ * Before the fill, option o of block s is dropped when an earlier option o' < o of the
+ * same block is at least as good in everything Eq. fe reads: r(F)+r(B), xbar and the
+ * memory the pair needs.  Then o' is a candidate wherever o is, never costs more (Opt is
+ * non-increasing in m) and wins ties by its smaller code, so every Opt value, every
+ * recorded choice and every schedule stay exactly as without the test; only the work
+ * shrinks.  Repeated options are the special case of equality.  Options and recorded
+ * choices always use the caller's option indices.
+ *
+ * rk_set_option_pruning: on (non-zero, the default) or off (every option evaluated, for
+ * measurement); takes effect at the next solve.
+ * rk_chain_options: kept[s*K + o] (host, [L*K], may be NULL) = 1 when option o of block
+ * s is evaluated under the current setting; *k_run (may be NULL) = option slots per block
+ * the kernels evaluate, the largest kept count (blocks with fewer are padded with slots
+ * that never win).  Does not touch the GPU.
+ */
+int rk_set_option_pruning(rk_chain *c, int32_t enable);
+int rk_chain_options(const rk_chain *c, int32_t *kept, int32_t *k_run);
 
 /* Short English description of an RK_* code. */
 const char *rk_strerror(int code);

@@ -28,7 +28,8 @@ import hashlib
 
 import numpy as np
 
-__all__ = ["Chain", "CONFIGS", "make_config_chain", "make_random_chain", "config_by_name"]
+__all__ = ["Chain", "CONFIGS", "make_config_chain", "make_random_chain", "make_grid_chain",
+           "config_by_name"]
 
 
 @dataclasses.dataclass
@@ -198,6 +199,66 @@ def make_random_chain(seed: int, L: int, K: int, *, M: int | None = None, xmax: 
         M = int(x.sum() + mem.max(axis=1).sum() + tf.max() + tb.max() + 2)
     return Chain(L=L, K=K, x=_i32(x), fn_time=fn_time, fn_tmp=fn_tmp, fwd=fwd, bwd=bwd,
                  mem=mem, tmp_fwd=tf, tmp_bwd=tb, M=int(M), name=f"random{seed}_L{L}_K{K}")
+
+
+def _grid_options(rng, n_peak: int, n_save: int):
+    """Per-option costs of one block type from an emulated option search on a budget grid.
+
+    Stand-in for the paper's block-level solver (Sec. 3, Phase 2), which is not part of this
+    build: a block produces n tensors, tensor j of size sz_j costing rc_j to compute; a few
+    are cheap to recompute and large (dropout/gelu-like), the rest costly.  A block schedule
+    keeps a subset S of them from the forward to the backward and recomputes the others
+    there.  For each pair (M_peak, M_save) of the grid (M_peak evenly spaced between the
+    peaks of keeping nothing and keeping everything, M_save evenly spaced in [0, M_peak]),
+    the subset with the least recomputation whose kept size fits M_save and whose backward
+    peak (kept size + the largest recomputed tensor + a workspace) fits M_peak is taken, by
+    enumeration.  Options come in grid order; different pairs often give the same subset.
+    """
+    n = int(rng.integers(6, 11))
+    cheap = rng.random(n) < 0.35
+    sz = np.where(cheap, rng.integers(8, 25, size=n), rng.integers(2, 12, size=n))
+    rc = np.where(cheap, rng.integers(1, 6, size=n), rng.integers(40, 250, size=n))
+    work = int(rng.integers(1, 6))
+    masks = np.arange(1 << n)
+    bits = (masks[:, None] >> np.arange(n)[None, :]) & 1
+    kept_size = bits @ sz
+    recompute = (1 - bits) @ rc
+    tmp_b = work + np.where(bits.all(axis=1), 0, ((1 - bits) * sz[None, :]).max(axis=1))
+    peak = kept_size + tmp_b
+    f = int(rc.sum())
+    lo, hi = int(peak[0]), int(peak[-1])
+    opts = []
+    for mp in np.linspace(lo, max(lo, hi), n_peak):
+        for ms in np.linspace(0, mp, n_save):
+            ok = (kept_size <= ms) & (peak <= mp)
+            ok[0] = True  # keeping nothing always fits: M_peak >= its peak
+            key = np.where(ok, recompute, np.iinfo(np.int64).max)
+            best = np.flatnonzero(key == key.min())
+            j = best[np.argmin(kept_size[best])]
+            opts.append((f, 2 * f + int(recompute[j]), int(kept_size[j]), work, int(tmp_b[j])))
+    return f, work, np.array(opts, dtype=np.int64)
+
+
+def make_grid_chain(seed: int, L: int, n_peak: int = 20, n_save: int = 20, *, types: int = 2,
+                    M: int | None = None, xmax: int = 6) -> Chain:
+    """A chain of `types` block types repeated in turn (GPT-like: attention and MLP blocks),
+    each with the n_peak * n_save options of an emulated grid search (see _grid_options);
+    identical blocks share their options, as in the paper.  Many options are repeats."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    tys = [_grid_options(rng, n_peak, n_save) for _ in range(types)]
+    x = rng.integers(1, xmax, size=L + 1, endpoint=True)
+    K = n_peak * n_save
+    fwd, bwd, mem, tf, tb = (np.empty((L, K), dtype=np.int64) for _ in range(5))
+    fn_time, fn_tmp = np.empty(L, dtype=np.int64), np.empty(L, dtype=np.int64)
+    for i in range(L):
+        f, work, o = tys[i % types]
+        fwd[i], bwd[i], mem[i], tf[i], tb[i] = o.T
+        fn_time[i], fn_tmp[i] = f, work
+    if M is None:
+        M = int((x.sum() + mem.max(axis=1).sum()) // 3)
+    return Chain(L=L, K=K, x=_i32(x), fn_time=_i32(fn_time), fn_tmp=_i32(fn_tmp), fwd=_i32(fwd),
+                 bwd=_i32(bwd), mem=_i32(mem), tmp_fwd=_i32(tf), tmp_bwd=_i32(tb), M=M,
+                 name=f"grid_L{L}_K{K}_s{seed}")
 
 
 def store_all_bound(ch: Chain) -> int:

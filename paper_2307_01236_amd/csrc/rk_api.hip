@@ -15,10 +15,18 @@ using rk::DINF;
 
 struct rk_chain {
     int32_t L = 0, K = 0;
-    std::vector<int32_t> x, xbar, c1, need1, need1max, P, need2;  // host copies of the device arrays
+    std::vector<int32_t> x, xbar, c1, need1, P, need2;  // derived per block and option, per split
+    // Options the kernels evaluate: per block, in the caller's order, the options kept by the
+    // dominance test (all of them when pruning is off), padded to k_run slots per block.
+    // run_opt maps a slot back to the caller's option index (-1 for padding).  These are the
+    // arrays on the device; run_prune is the setting they were built with.
+    std::vector<uint8_t> kept;  // [L*K] option survives the dominance test
+    bool prune = true, run_prune = true;
+    int32_t k_run = 0;
+    std::vector<int32_t> run_opt, run_xbar, run_c1, run_need1, run_need1max;
 
     int device = -1;
-    void *d_chain = nullptr;  // x | xbar | c1 | need1 | P | need2
+    void *d_chain = nullptr;  // x | xbar | c1 | need1 | need1max | P | need2 (options: run arrays)
     DevChain dc{};
 
     int32_t max_x = 0;       // largest x_i over the split points i = 1..L-1
@@ -103,11 +111,62 @@ int geometry(const rk_chain *c, int32_t M, Geometry *g, size_t *bytes)
     return RK_OK;
 }
 
-// First solve on a device: upload the derived arrays and create the events.
+// Option slots of every block for the kernels: the kept options (every option when pruning
+// is off) in the caller's order, then padding up to the largest count.  A padding slot costs
+// the device infinity and needs only x_{s+1}: wherever it is a candidate its value is at or
+// above infinity, so it never changes a minimum and is never the recorded choice.
+void build_run(rk_chain *c)
+{
+    const int32_t L = c->L, K = c->K;
+    c->run_prune = c->prune;
+    int32_t kr = 1;
+    for (int32_t s = 0; s < L; ++s) {
+        int32_t n = 0;
+        for (int32_t o = 0; o < K; ++o) n += !c->prune || c->kept[(size_t)s * K + o];
+        kr = std::max(kr, n);
+    }
+    c->k_run = kr;
+    const size_t nr = (size_t)L * kr;
+    c->run_opt.assign(nr, -1);
+    c->run_xbar.assign(nr, 0);
+    c->run_c1.assign(nr, DINF);
+    c->run_need1.assign(nr, 0);
+    c->run_need1max.assign(L, 0);
+    for (int32_t s = 0; s < L; ++s) {
+        int32_t slot = 0;
+        for (int32_t o = 0; o < K; ++o) {
+            const size_t j = (size_t)s * K + o;
+            if (c->prune && !c->kept[j]) continue;
+            const size_t r = (size_t)s * kr + slot++;
+            c->run_opt[r] = o;
+            c->run_xbar[r] = c->xbar[j];
+            c->run_c1[r] = c->c1[j];
+            c->run_need1[r] = c->need1[j];
+            c->run_need1max[s] = std::max(c->run_need1max[s], c->need1[j]);
+        }
+        for (; slot < kr; ++slot) {
+            const size_t r = (size_t)s * kr + slot;
+            c->run_xbar[r] = c->run_need1[r] = c->x[s + 1];
+        }
+    }
+}
+
+// First solve on a device (or the first after the pruning switch changed): upload the
+// derived arrays; create the events and streams once.
 int ensure_device(rk_chain *c)
 {
-    if (c->d_chain) return RK_OK;
-    const int32_t L = c->L, K = c->K;
+    if (c->d_chain && c->run_prune == c->prune) return RK_OK;
+    if (c->d_chain) {  // rebuild: the captured launch sequence holds the old arrays
+        if (c->queued) HIPCHK(hipEventSynchronize(c->ev_fill1));
+        HIPCHK(hipFree(c->d_chain));
+        c->d_chain = nullptr;
+        if (c->gexec) (void)hipGraphExecDestroy(c->gexec);
+        c->gexec = nullptr;
+        c->queued = false;
+        c->bt_fill = -1;
+    }
+    build_run(c);
+    const int32_t L = c->L, K = c->k_run;
     const size_t nx = L + 1, nk = (size_t)L * K, nl = (size_t)L * L;
     const size_t total = nx + 3 * nk + L + 2 * nl;
     HIPCHK(hipMalloc(&c->d_chain, total * sizeof(int32_t)));
@@ -123,22 +182,24 @@ int ensure_device(rk_chain *c)
     c->dc.L = L;
     c->dc.K = K;
     c->dc.x = put(c->x);
-    c->dc.xbar = put(c->xbar);
-    c->dc.c1 = put(c->c1);
-    c->dc.need1 = put(c->need1);
-    c->dc.need1max = put(c->need1max);
+    c->dc.xbar = put(c->run_xbar);
+    c->dc.c1 = put(c->run_c1);
+    c->dc.need1 = put(c->run_need1);
+    c->dc.need1max = put(c->run_need1max);
     c->dc.P = put(c->P);
     c->dc.need2 = put(c->need2);
     int64_t xbar_max = 0;
-    for (int32_t v : c->xbar) xbar_max = std::max<int64_t>(xbar_max, v);
+    for (int32_t v : c->run_xbar) xbar_max = std::max<int64_t>(xbar_max, v);
     c->dc.xbar_halo = xbar_max > rk::HMAX ? rk::HMAX + 1 : rk::round64(xbar_max);
     if (!c->dc.x || !c->dc.xbar || !c->dc.c1 || !c->dc.need1 || !c->dc.need1max || !c->dc.P ||
         !c->dc.need2)
         return RK_E_DEVICE;
-    HIPCHK(hipEventCreate(&c->ev_fill0));
-    HIPCHK(hipEventCreate(&c->ev_fill1));
-    HIPCHK(hipStreamCreateWithFlags(&c->own_stream, hipStreamNonBlocking));
-    HIPCHK(hipMalloc(&c->d_res, 4 * sizeof(int64_t)));
+    if (!c->ev_fill0) {
+        HIPCHK(hipEventCreate(&c->ev_fill0));
+        HIPCHK(hipEventCreate(&c->ev_fill1));
+        HIPCHK(hipStreamCreateWithFlags(&c->own_stream, hipStreamNonBlocking));
+        HIPCHK(hipMalloc(&c->d_res, 4 * sizeof(int64_t)));
+    }
     return RK_OK;
 }
 
@@ -256,7 +317,7 @@ int rk_chain_create(int32_t L, int32_t K, const int32_t *x, const int32_t *fn_ti
         c->xbar.resize(nk);
         c->c1.resize(nk);
         c->need1.resize(nk);
-        c->need1max.assign(L, 0);
+        c->kept.assign(nk, 1);
         c->P.assign((size_t)L * L, 0);
         c->need2.assign((size_t)L * L, 0);
     } catch (...) {
@@ -272,7 +333,23 @@ int rk_chain_create(int32_t L, int32_t K, const int32_t *x, const int32_t *fn_ti
             c->xbar[j] = (int32_t)std::min(xb, kSizeCap);
             c->need1[j] = (int32_t)std::min(xb + std::max(tmp_fwd[j], tmp_bwd[j]), kSizeCap);
             c->c1[j] = fwd[j] + bwd[j];
-            c->need1max[s] = std::max(c->need1max[s], c->need1[j]);
+        }
+    // Option o of block s is never the recorded choice when an earlier option o' < o of the
+    // block is at least as good in all that Eq. fe reads: r(F)+r(B), xbar and the memory the
+    // pair needs.  Then o' is a candidate wherever o is, and (Opt being non-increasing in m)
+    // never costs more; at equal cost it wins by its smaller code.  Testing against the kept
+    // options suffices: dominance is transitive.  This also drops repeated options, which the
+    // paper's budget grid produces many of (Sec. 3, Phase 2).
+    for (int32_t s = 0; s < L; ++s)
+        for (int32_t o = 1; o < K; ++o) {
+            const int64_t j = (int64_t)s * K + o;
+            for (int32_t q = 0; q < o; ++q) {
+                const int64_t i = (int64_t)s * K + q;
+                if (c->kept[i] && c->c1[i] <= c->c1[j] && c->xbar[i] <= c->xbar[j] && c->need1[i] <= c->need1[j]) {
+                    c->kept[j] = 0;
+                    break;
+                }
+            }
         }
     // Case 2 (Eq. fn): the sweep F_s^0..F_{i-1}^0 costs P[s][i]; F_k^0 holds its input
     // (except the span input x_s, outside the budget), its output and tmp(F_k^0).
@@ -403,6 +480,9 @@ int rk_extract_schedule(rk_chain *c, rk_op *ops, int64_t cap, int64_t *n_ops, in
     if (n_fwd) *n_fwd = res[1];
     if (!ops || cap < res[0]) return RK_E_BUFSZ;
     HIPCHK(hipMemcpy(ops, c->d_ops, res[0] * sizeof(rk_op), hipMemcpyDeviceToHost));
+    for (int64_t k = 0; k < res[0]; ++k)  // option slots back to the caller's option indices
+        if (ops[k].kind == RK_FWD_SAVE || ops[k].kind == RK_BWD)
+            ops[k].option = c->run_opt[(size_t)ops[k].block * c->k_run + ops[k].option];
     return RK_OK;
 }
 
@@ -430,6 +510,8 @@ int rk_read_row(rk_chain *c, int32_t s, int32_t t, int32_t *opt_row, int16_t *ar
         HIPCHK(hipMemcpyAsync(arg_row, c->d_argrow, (size_t)c->W * sizeof(int16_t),
                               hipMemcpyDeviceToHost, c->stream));
         HIPCHK(hipStreamSynchronize(c->stream));
+        for (int32_t m = 0; m < c->W; ++m)  // option slots back to the caller's option indices
+            if (arg_row[m] >= c->L) arg_row[m] = (int16_t)(c->L + c->run_opt[(size_t)s * c->k_run + (arg_row[m] - c->L)]);
     }
     return RK_OK;
 }
@@ -496,6 +578,31 @@ int rk_fill_kernel_stats(rk_chain *c, int32_t kind, int32_t *n_kinds, const char
     if (total_ms) *total_ms = sum;
     if (relaxations) *relaxations = c->prof.work[kind];
     if (bytes) *bytes = c->prof.bytes[kind];
+    return RK_OK;
+}
+
+int rk_set_option_pruning(rk_chain *c, int32_t enable)
+{
+    if (!c) return RK_E_INVAL;
+    c->prune = enable != 0;
+    return RK_OK;
+}
+
+int rk_chain_options(const rk_chain *c, int32_t *kept, int32_t *k_run)
+{
+    if (!c) return RK_E_INVAL;
+    int32_t kr = 1;
+    for (int32_t s = 0; s < c->L; ++s) {
+        int32_t n = 0;
+        for (int32_t o = 0; o < c->K; ++o) {
+            const size_t j = (size_t)s * c->K + o;
+            const int32_t v = !c->prune || c->kept[j];
+            if (kept) kept[j] = v;
+            n += v;
+        }
+        kr = std::max(kr, n);
+    }
+    if (k_run) *k_run = kr;
     return RK_OK;
 }
 

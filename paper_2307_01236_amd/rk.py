@@ -24,7 +24,7 @@ RK_FWD_NOSAVE, RK_FWD_SAVE, RK_BWD, RK_FREE_X = 0, 1, 2, 3
 
 EXPORTS = ("rk_chain_create", "rk_chain_destroy", "rk_workspace_bytes", "rk_solve", "rk_solve_async",
            "rk_result", "rk_extract_schedule", "rk_read_row", "rk_tradeoff_curve", "rk_last_fill_ms",
-           "rk_set_profiling",
+           "rk_set_profiling", "rk_set_option_pruning", "rk_chain_options",
            "rk_fill_kernel_stats", "rk_strerror")
 
 
@@ -66,6 +66,8 @@ def load():
         lib.rk_tradeoff_curve.argtypes = [C.c_void_p, i32p, i64]
         lib.rk_last_fill_ms.argtypes = [C.c_void_p, P(C.c_float), i32p]
         lib.rk_set_profiling.argtypes = [C.c_void_p, i32]
+        lib.rk_set_option_pruning.argtypes = [C.c_void_p, i32]
+        lib.rk_chain_options.argtypes = [C.c_void_p, i32p, i32p]
         lib.rk_fill_kernel_stats.argtypes = [C.c_void_p, i32, i32p, P(C.c_char_p), i32p,
                                              P(C.c_float), P(i64), P(i64)]
         lib.rk_strerror.argtypes = [C.c_int]
@@ -164,6 +166,19 @@ def rk_last_fill_ms(h):
     return float(ms.value), int(n.value)
 
 
+def rk_set_option_pruning(h, enable: bool) -> None:
+    _check(load().rk_set_option_pruning(h, 1 if enable else 0), "rk_set_option_pruning")
+
+
+def rk_chain_options(h, L: int, K: int):
+    """(kept [L, K] bool, k_run): which options the solver evaluates, and slots per block."""
+    kept = np.empty(L * K, dtype=np.int32)
+    kr = C.c_int32(0)
+    _check(load().rk_chain_options(h, kept.ctypes.data_as(C.POINTER(C.c_int32)), C.byref(kr)),
+           "rk_chain_options")
+    return kept.reshape(L, K).astype(bool), int(kr.value)
+
+
 def rk_set_profiling(h, enable: bool) -> None:
     _check(load().rk_set_profiling(h, 1 if enable else 0), "rk_set_profiling")
 
@@ -208,6 +223,13 @@ class Solver:
 
     def schedule(self):
         return rk_extract_schedule(self.h)
+
+    def set_option_pruning(self, enable: bool) -> None:
+        rk_set_option_pruning(self.h, enable)
+
+    def options(self):
+        """(kept [L, K] bool, k_run) under the current pruning setting."""
+        return rk_chain_options(self.h, self.L, self.K)
 
     def row(self, s: int, t: int, want_arg: bool = True):
         return rk_read_row(self.h, s, t, self.M + 1, want_arg)

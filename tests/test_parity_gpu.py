@@ -12,8 +12,8 @@ import pytest
 
 import oracle
 from paper_2307_01236_amd import rk
-from paper_2307_01236_amd.chaingen import (CONFIGS, make_config_chain, make_random_chain,
-                                            relaxations, store_all_bound)
+from paper_2307_01236_amd.chaingen import (CONFIGS, make_config_chain, make_grid_chain,
+                                            make_random_chain, relaxations, store_all_bound)
 
 pytestmark = pytest.mark.gpu
 INF = rk.RK_INF
@@ -24,13 +24,14 @@ def say(*a):
     sys.stdout.flush()
 
 
-def full_parity(ch, M=None, check_schedule=True):
+def full_parity(ch, M=None, check_schedule=True, prune=True):
     """Whole Opt and choice tables, the answer and the schedule."""
     M = ch.M if M is None else M
-    say(f"  full parity {ch.name} L={ch.L} K={ch.K} M={M}")
+    say(f"  full parity {ch.name} L={ch.L} K={ch.K} M={M} pruning={prune}")
     sol = oracle.solve(ch, M)
     s = rk.Solver(ch)
     try:
+        s.set_option_pruning(prune)
         ans = s.solve(M)
         assert ans == sol.answer, (ans, sol.answer)
         g_opt, g_arg = s.rows()
@@ -310,5 +311,37 @@ def test_tradeoff_curve_errors():
             s.tradeoff_curve(ch.M + 2)
         assert e.value.code == rk.RK_E_INVAL
         assert s.tradeoff_curve(0).size == 0
+    finally:
+        s.close()
+
+
+@pytest.mark.parametrize("prune", [True, False])
+def test_grid_options_pruned_and_unpruned(prune):
+    """An emulated budget-grid option search (100 options per block, mostly repeats, three
+    block types): with pruning the kernels evaluate only the distinct options; tables,
+    choices (in the caller's option indices) and the schedule match the oracle exactly
+    either way."""
+    ch = make_grid_chain(5, 24, 10, 10, types=3)
+    full_parity(ch, prune=prune)
+
+
+def test_pruning_switch_between_solves():
+    """Turning pruning off and on between solves of one chain rebuilds the device arrays and
+    the captured launch sequence; every solve still matches the oracle."""
+    ch = make_grid_chain(6, 20, 8, 8)
+    sol = oracle.solve(ch)
+    o_opt, o_arg = sol.rows()
+    exp = oracle.schedule(sol)
+    s = rk.Solver(ch)
+    try:
+        for prune in (True, False, True):
+            s.set_option_pruning(prune)
+            assert s.solve() == sol.answer
+            opt, arg = s.rows()
+            assert np.array_equal(opt, o_opt) and np.array_equal(arg, o_arg), prune
+            ops, nfwd = s.schedule()
+            assert np.array_equal(ops, exp[0]) and nfwd == exp[1]
+            kept, k_run = s.options()
+            assert (k_run < ch.K) == prune
     finally:
         s.close()
