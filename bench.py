@@ -2,9 +2,7 @@
 
 One step is one pass of the whole hot path over one chain: the table fill for
 every span and every budget (App. C, Alg. 2), the answer read-back, and the
-schedule (Alg. 3) copied to the host.  Outside the timed steps it also reports
-the memory/time trade-off curve of the fill against Rotor's (Sec. 4) and the
-effect of option pruning on a chain with an emulated budget-grid option search.  The chain is the deep transformer-like
+schedule (Alg. 3) copied to the host.  The chain is the deep transformer-like
 workload, 384 blocks with 16 options each at a 6000-slot budget, created and
 uploaded before the timed region; the table lives in a torch allocation and
 the solve runs on a torch stream.
@@ -17,7 +15,11 @@ stream) against the roof that binds it: HBM bandwidth for its compulsory table
 traffic (every row a launch reads counted once, plus the rows it writes) or the
 VALU integer peak for its relaxations (an add and a min each), whichever
 fraction is higher; the other one is reported beside it.  ``cpu_baseline``
-times the CPU oracle (one core) on a bounded part of the same chain.
+times the CPU oracle (one core) on a bounded part of the same chain.  After
+the timed and profiled steps, ``tradeoff`` and ``option_pruning`` report the
+memory/time trade-off curve of the fill against Rotor's (Sec. 4) and the effect
+of option pruning on a chain with an emulated budget-grid option search
+(``--extras 0`` skips both, for profiler runs that should see one workload).
 """
 from __future__ import annotations
 
@@ -77,6 +79,53 @@ def cpu_baseline(ch, nblocks: int):
             "seconds": dt}
 
 
+def extras(ch, s, M):
+    """Reports beside the benchmark: the trade-off curve against Rotor's and option pruning."""
+    from paper_2307_01236_amd import rk
+    from paper_2307_01236_amd.chaingen import make_grid_chain, relaxations
+
+    # Sec. 4's comparison with Rotor on the same chain: the trade-off curve of this fill (every
+    # budget's optimum) against one of Rotor's choice set (keep everything or nothing per
+    # block: option 0), as overhead over the time with no recomputation
+    t = time.perf_counter()
+    curve = s.tradeoff_curve()
+    curve_ms = (time.perf_counter() - t) * 1e3
+    rot = rk.Solver(ch.options([0]))
+    rot.solve(M)
+    rcurve = rot.tradeoff_curve()
+    rot.close()
+    ideal = int((ch.fwd.astype("int64") + ch.bwd).min(axis=1).sum())
+    budgets = [int(M * f) for f in (0.1, 0.2, 0.3, 0.5, 0.75, 1.0)]
+    ovh = lambda v: None if v == rk.RK_INF else round(int(v) / ideal - 1.0, 4)
+    tradeoff = {"curve_read_ms": curve_ms, "budgets": budgets,
+                "rk_rotor_overhead": [ovh(curve[b]) for b in budgets],
+                "rotor_overhead": [ovh(rcurve[b]) for b in budgets],
+                "min_budget_rk_rotor": int((curve < rk.RK_INF).argmax()),
+                "min_budget_rotor": int((rcurve < rk.RK_INF).argmax())}
+    log(f"trade-off: {tradeoff}")
+
+    # Option pruning (Sec. 3, Phase 2: the budget grid of the option search repeats options):
+    # an emulated 20 x 20 grid search gives 400 options per block on a 96-block chain; the
+    # fill with the distinct ones only against the fill with all of them
+    g = make_grid_chain(1, 96)
+    pruning = {"workload": g.name, "L": g.L, "K": g.K, "M": g.M}
+    gs = rk.Solver(g)
+    for on in (True, False):
+        gs.set_option_pruning(on)
+        k_run = gs.options()[1]
+        fills = []
+        for _ in range(4):
+            gs.solve(g.M)
+            fills.append(gs.fill_ms()[0])
+        key = "pruned" if on else "all_options"
+        pruning[key] = {"k_run": k_run, "fill_ms": statistics.median(fills[1:]),
+                        "relaxations": relaxations(g.L, k_run, g.M), "answer": gs.result()}
+    gs.close()
+    log(f"option pruning: {pruning}")
+
+    return tradeoff, pruning
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -84,6 +133,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=WORKLOAD_CFG)
     ap.add_argument("--cpu-blocks", type=int, default=96, help="oracle sample size (0: skip)")
+    ap.add_argument("--extras", type=int, default=1,
+                    help="0: skip the trade-off and option-pruning reports (other chains' fills)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized buffer 3 times (to scale HBM byte counters) and exit")
     args = ap.parse_args()
@@ -166,45 +217,9 @@ def main():
     s.schedule()
     sched_ms = (time.perf_counter() - t) * 1e3
 
-    # Sec. 4's comparison with Rotor on the same chain: the trade-off curve of this fill (every
-    # budget's optimum) against one of Rotor's choice set (keep everything or nothing per
-    # block: option 0), as overhead over the time with no recomputation
-    t = time.perf_counter()
-    curve = s.tradeoff_curve()
-    curve_ms = (time.perf_counter() - t) * 1e3
-    rot = rk.Solver(ch.options([0]))
-    rot.solve(M)
-    rcurve = rot.tradeoff_curve()
-    rot.close()
-    ideal = int((ch.fwd.astype("int64") + ch.bwd).min(axis=1).sum())
-    budgets = [int(M * f) for f in (0.1, 0.2, 0.3, 0.5, 0.75, 1.0)]
-    ovh = lambda v: None if v == rk.RK_INF else round(int(v) / ideal - 1.0, 4)
-    tradeoff = {"curve_read_ms": curve_ms, "budgets": budgets,
-                "rk_rotor_overhead": [ovh(curve[b]) for b in budgets],
-                "rotor_overhead": [ovh(rcurve[b]) for b in budgets],
-                "min_budget_rk_rotor": int((curve < rk.RK_INF).argmax()),
-                "min_budget_rotor": int((rcurve < rk.RK_INF).argmax())}
-    log(f"trade-off: {tradeoff}")
-
-    # Option pruning (Sec. 3, Phase 2: the budget grid of the option search repeats options):
-    # an emulated 20 x 20 grid search gives 400 options per block on a 96-block chain; the
-    # fill with the distinct ones only against the fill with all of them
-    from paper_2307_01236_amd.chaingen import make_grid_chain
-    g = make_grid_chain(1, 96)
-    pruning = {"workload": g.name, "L": g.L, "K": g.K, "M": g.M}
-    gs = rk.Solver(g)
-    for on in (True, False):
-        gs.set_option_pruning(on)
-        k_run = gs.options()[1]
-        fills = []
-        for _ in range(4):
-            gs.solve(g.M)
-            fills.append(gs.fill_ms()[0])
-        key = "pruned" if on else "all_options"
-        pruning[key] = {"k_run": k_run, "fill_ms": statistics.median(fills[1:]),
-                        "relaxations": relaxations(g.L, k_run, g.M), "answer": gs.result()}
-    gs.close()
-    log(f"option pruning: {pruning}")
+    tradeoff = pruning = None
+    if args.extras:  # other chains' fills: after the timed and profiled steps
+        tradeoff, pruning = extras(ch, s, M)
 
     # dominant kernel: the one with the most device time; both of its roofs per launch
     dname, (dn, dms, dwork, dbytes) = max(kern.items(), key=lambda kv: kv[1][1])
