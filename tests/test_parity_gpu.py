@@ -345,3 +345,33 @@ def test_pruning_switch_between_solves():
             assert (k_run < ch.K) == prune
     finally:
         s.close()
+
+
+def test_backtrace_with_option_sizes_in_global_memory():
+    """400 options per block on 36 blocks, pruning off: L*K = 14400 option sizes do not fit the
+    backtrace's LDS copy, so it reads them from global memory, and a visited cell's options
+    take seven rounds of lanes.  Tables and schedule still match the oracle exactly."""
+    ch = make_grid_chain(8, 36, 20, 20)
+    full_parity(ch, prune=False)
+
+
+def test_longest_chain():
+    """RK_MAX_L = 2000 blocks (1999 finalize launches; a backtrace whose LDS stack of up to
+    2L + 8 frames and x copy take 72 KB).  Exact parity on sub-chains at both ends; the
+    schedule replays legally in the oracle's simulator at exactly the answer and within the
+    budget (the oracle's full table would take minutes; the simulator shares nothing with it)."""
+    L = rk.RK_MAX_L
+    ch = make_random_chain(2024, L, 2, M=600, xmax=3, amax=4, tmax=2, small_times=True)
+    s = rk.Solver(ch)
+    try:
+        ans = s.solve()
+        assert ans != INF
+        for s0 in (0, L - 14):
+            sub_rows_parity(s, ch, s0, 14)
+        ops, nfwd = s.schedule()
+        ok, tm, pk, bad = oracle.simulate(ch, ops)
+        assert ok, bad
+        assert tm == ans and pk <= ch.M
+        assert ops[nfwd][0] == rk.RK_BWD
+    finally:
+        s.close()
