@@ -192,13 +192,18 @@ int ensure_device(rk_chain *c)
     for (int32_t v : c->run_xbar) xbar_max = std::max<int64_t>(xbar_max, v);
     c->dc.xbar_halo = xbar_max > rk::HMAX ? rk::HMAX + 1 : rk::round64(xbar_max);
     if (!c->dc.x || !c->dc.xbar || !c->dc.c1 || !c->dc.need1 || !c->dc.need1max || !c->dc.P ||
-        !c->dc.need2)
+        !c->dc.need2) {  // leave no half-uploaded arrays behind: the next solve uploads again
+        (void)hipFree(c->d_chain);
+        c->d_chain = nullptr;
         return RK_E_DEVICE;
-    if (!c->ev_fill0) {
-        HIPCHK(hipEventCreate(&c->ev_fill0));
-        HIPCHK(hipEventCreate(&c->ev_fill1));
-        HIPCHK(hipStreamCreateWithFlags(&c->own_stream, hipStreamNonBlocking));
-        HIPCHK(hipMalloc(&c->d_res, 4 * sizeof(int64_t)));
+    }
+    // each created once; a call that failed half way creates the rest next time
+    if (!c->ev_fill0) HIPCHK(hipEventCreate(&c->ev_fill0));
+    if (!c->ev_fill1) HIPCHK(hipEventCreate(&c->ev_fill1));
+    if (!c->own_stream) HIPCHK(hipStreamCreateWithFlags(&c->own_stream, hipStreamNonBlocking));
+    if (!c->d_res && hipMalloc(&c->d_res, 4 * sizeof(int64_t)) != hipSuccess) {
+        c->d_res = nullptr;
+        return RK_E_NOMEM;
     }
     return RK_OK;
 }
@@ -371,10 +376,10 @@ int rk_chain_create(int32_t L, int32_t K, const int32_t *x, const int32_t *fn_ti
 void rk_chain_destroy(rk_chain *c)
 {
     if (!c) return;
-    if (c->d_chain) {
+    if (c->device >= 0) {  // something may live on the chain's device
         DeviceScope ds(c);
         if (c->queued && c->ev_fill1) (void)hipEventSynchronize(c->ev_fill1);
-        (void)hipFree(c->d_chain);
+        if (c->d_chain) (void)hipFree(c->d_chain);
         if (c->own_ws) (void)hipFree(c->own_ws);
         if (c->d_ops) (void)hipFree(c->d_ops);
         if (c->d_res) (void)hipFree(c->d_res);
