@@ -14,7 +14,9 @@ kind with the most device time, from per-launch HIP events on the solve's
 stream) against the roof that binds it: HBM bandwidth for its compulsory table
 traffic (every row a launch reads counted once, plus the rows it writes) or the
 VALU integer peak for its relaxations (an add and a min each), whichever
-fraction is higher; the other one is reported beside it.  ``cpu_baseline``
+fraction is higher; the other one is reported beside it; both are also priced
+against what this GPU sustains (``measured_ceilings``: int32 add/min chains over
+the whole chip, a 1 GiB device copy).  ``cpu_baseline``
 times the CPU oracle (one core) on a bounded part of the same chain.  After
 the timed and profiled steps, ``tradeoff`` and ``option_pruning`` report the
 memory/time trade-off curve of the fill against Rotor's (Sec. 4) and the effect
@@ -242,6 +244,17 @@ def main():
                                 / VALU_PEAK_TOPS,
     })
 
+    # what this GPU sustains, next to the published peaks: int32 add+min chains over the
+    # whole chip, and a 1 GiB device copy (bytes read plus written)
+    from paper_2307_01236_amd import calib
+    measured = {"valu_int32_tops": calib.valu_int32_rate() / 1e12,
+                "copy_gbs": calib.copy_bandwidth(1 << 30) / 1e9}
+    log(f"measured ceilings: {measured}")
+    for r in (roofline, roofline["other_roof"]):
+        mp = measured["copy_gbs"] if r["bound"] == "hbm" else measured["valu_int32_tops"]
+        r["measured_peak"] = mp
+        r["frac_of_measured"] = r["achieved"] / mp
+
     cpu = None
     if args.cpu_blocks > 0:
         log(f"cpu baseline: oracle on {args.cpu_blocks} blocks ...")
@@ -258,7 +271,8 @@ def main():
         "wall_solve_ms": statistics.median(wall), "fill_ms": statistics.median(fill_ms),
         "schedule_ms": sched_ms,
         "fill_relax_per_s": relax / (statistics.median(fill_ms) * 1e-3),
-        "roofline": roofline, "cpu_baseline": cpu, "tradeoff": tradeoff, "option_pruning": pruning,
+        "roofline": roofline, "measured_ceilings": measured, "cpu_baseline": cpu, "tradeoff": tradeoff,
+        "option_pruning": pruning,
         "kernels": {k: {"launches_per_step": v[0] / args.steps, "ms_per_step": v[1] / args.steps,
                         "relaxations_per_step": v[2] // args.steps, "table_bytes_per_step": v[3] // args.steps}
                     for k, v in kern.items()},

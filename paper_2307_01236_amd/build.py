@@ -1,4 +1,5 @@
-"""Build librkrotor.so (HIP, gfx950) in-tree with hipcc."""
+"""Build librkrotor.so (the solver) and librkcalib.so (measured GPU ceilings for the
+benchmark), HIP for gfx950, in-tree with hipcc."""
 from __future__ import annotations
 
 import os
@@ -11,6 +12,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "librkrotor.so")
 SOURCES = ["rk_api.hip", "rk_kernels.hip"]
+CALIB_LIB = os.path.join(PKG, "librkcalib.so")
+CALIB_SOURCES = ["rk_calib.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -28,9 +31,9 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build(verbose: bool = False) -> str:
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    tmp = LIB + ".tmp"
+def _compile(sources, out: str, verbose: bool) -> str:
+    srcs = [os.path.join(CSRC, s) for s in sources]
+    tmp = out + ".tmp"
     cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), "-I", CSRC, *srcs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -38,8 +41,14 @@ def build(verbose: bool = False) -> str:
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
         raise RuntimeError(f"hipcc failed ({res.returncode})")
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
+
+
+def build(verbose: bool = False) -> str:
+    """Both libraries; returns the solver's path."""
+    _compile(CALIB_SOURCES, CALIB_LIB, verbose)
+    return _compile(SOURCES, LIB, verbose)
 
 
 if __name__ == "__main__":

@@ -27,6 +27,23 @@ def test_exports_every_declared_symbol():
     assert set(names) == set(rk.EXPORTS)
 
 
+def test_calibration_library_exports():
+    from paper_2307_01236_amd import calib
+    text = open(os.path.join(ROOT, "include", "rk_calib.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = sorted(set(re.findall(r"\b(rkc_[a-z0-9_]+)\s*\(", text)))
+    assert set(names) == set(calib.EXPORTS)
+    lib = calib.load()
+    for n in names:
+        assert hasattr(lib, n), n
+    # argument checks happen before any device call
+    import ctypes as C
+    out = C.c_double()
+    assert lib.rkc_valu_int32_rate(0, C.byref(out)) == -1
+    assert lib.rkc_copy_bandwidth(17, C.byref(out)) == -1
+    assert lib.rkc_copy_bandwidth(1 << 30, None) == -1
+
+
 def test_constants_match_header():
     text = open(os.path.join(ROOT, "include", "rk.h")).read()
     for name in ("RK_OK", "RK_E_INVAL", "RK_E_OVERFLOW", "RK_E_NOMEM", "RK_E_DEVICE", "RK_E_NOT_SOLVED",

@@ -1,0 +1,17 @@
+"""The measured-ceiling calls of librkcalib on an MI355X: plausible against the published
+peaks (int32 VALU 256 CU x 64 lanes x 2.4 GHz; HBM 8 TB/s)."""
+import pytest
+
+from paper_2307_01236_amd import calib
+
+pytestmark = pytest.mark.gpu
+
+
+def test_valu_rate_below_nominal_peak():
+    r = calib.valu_int32_rate(1 << 12)
+    assert 0.3 * 39.3e12 < r < 1.05 * 39.3e12, r
+
+
+def test_copy_bandwidth_below_hbm_peak():
+    bw = calib.copy_bandwidth(1 << 28)
+    assert 1e12 < bw < 8.0e12, bw
