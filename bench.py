@@ -75,10 +75,16 @@ def cpu_baseline(ch, nblocks: int):
     oracle.solve(sub)
     dt = time.perf_counter() - t0
     r = relaxations(sub.L, sub.K, sub.M)
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), model)
+    except OSError:
+        pass
     return {"value": r / dt, "unit": "relaxations/s", "cores": 1, "kind": "oracle",
             "sample": f"blocks 0..{nblocks - 1} of the same chain, M={sub.M}: {r:.3e} relaxations "
                       f"in {dt:.2f} s on one host core",
-            "seconds": dt}
+            "seconds": dt, "cpu_model": model, "host_cpus": os.cpu_count()}
 
 
 def extras(ch, s, M):
@@ -134,7 +140,7 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=WORKLOAD_CFG)
-    ap.add_argument("--cpu-blocks", type=int, default=96, help="oracle sample size (0: skip)")
+    ap.add_argument("--cpu-blocks", type=int, default=144, help="oracle sample size (0: skip)")
     ap.add_argument("--extras", type=int, default=1,
                     help="0: skip the trade-off and option-pruning reports (other chains' fills)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -166,6 +172,14 @@ def main():
     relax = relaxations(ch.L, ch.K, M)
     ncells = cells(ch.L, M)
     log(f"workload {ch.name}: L={ch.L} K={ch.K} M={M} relaxations={relax:.3e} sha={ch.sha256()[:16]}")
+
+    # cold first solve: a fresh chain handle uploads its arrays, allocates its table, captures
+    # the fill's launch sequence and runs it (synchronous rk_solve)
+    t = time.perf_counter()
+    cold = rk.Solver(ch)
+    cold.solve(M)
+    cold_ms = (time.perf_counter() - t) * 1e3
+    cold.close()
 
     s = rk.Solver(ch)
     nbytes = s.workspace_bytes(M)
@@ -268,7 +282,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": ch.name, "L": ch.L, "K": ch.K, "M": M, "relaxations": relax,
                    "cells": ncells, "chain_sha256": ch.sha256(), "answer": ans, "schedule_ops": nops},
-        "wall_solve_ms": statistics.median(wall), "fill_ms": statistics.median(fill_ms),
+        "wall_solve_ms": statistics.median(wall), "cold_solve_ms": cold_ms, "fill_ms": statistics.median(fill_ms),
         "schedule_ms": sched_ms,
         "fill_relax_per_s": relax / (statistics.median(fill_ms) * 1e-3),
         "roofline": roofline, "measured_ceilings": measured, "cpu_baseline": cpu, "tradeoff": tradeoff,
