@@ -110,10 +110,16 @@ int rk_solve(rk_chain *c, int32_t M, int32_t *opt_out);
  * stream a hipStream_t (NULL: a stream the chain owns).  Returns once the work
  * is queued.  The fill's kernel sequence is captured into a HIP graph on first
  * use and replayed while M, the workspace, the stream and the profiling switch
- * stay the same; on a stream the caller is itself capturing, the kernels are
- * launched directly (and become part of the caller's graph).  The workspace must stay allocated and untouched until the chain is
- * destroyed or solved again; the chain reads results from it.  Call
+ * stay the same.  The workspace must stay allocated and untouched until the
+ * chain is destroyed or solved again; the chain reads results from it.  Call
  * rk_result to wait and read the answer.
+ *
+ * On a stream the caller is capturing into a HIP graph, the kernels are launched
+ * directly and become part of the caller's graph; nothing is allocated, uploaded or
+ * waited on.  That needs a chain solved once before (outside the capture, with the
+ * same option-pruning setting), a caller workspace, and profiling off, else
+ * RK_E_INVAL.  Each replay of the caller's graph refills the table; rk_result and the
+ * reads then return the last replay's results once it has run.
  */
 int rk_solve_async(rk_chain *c, int32_t M, void *d_workspace, size_t ws_bytes, void *stream);
 

@@ -210,7 +210,10 @@ int ensure_device(rk_chain *c)
 
 int32_t to_abi(int32_t v) { return v >= DINF ? RK_INF : v; }
 
-int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t stream)
+// Queue the fill on `stream`: replay the captured launch sequence when nothing it depends
+// on changed, else capture it anew; inside a capture of the caller's (in_capture) the
+// kernels are launched directly into that capture.
+int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t stream, bool in_capture = false)
 {
     c->queued = false;
     c->M = M;
@@ -225,7 +228,10 @@ int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t
     HIPCHK(hipEventRecord(c->ev_fill0, stream));
     const bool replay = c->gexec && c->g_M == M && c->g_tables == tables && c->g_stream == stream &&
                         c->g_prof == c->prof.on;
-    if (replay) {
+    if (in_capture) {
+        c->prof.reset(stream);
+        HIPCHK(rk::launch_fill(c->dc, c->tb, stream, &c->launches, &c->prof));
+    } else if (replay) {
         HIPCHK(hipGraphLaunch(c->gexec, stream));
     } else {
         if (c->gexec) (void)hipGraphExecDestroy(c->gexec);
@@ -409,6 +415,15 @@ int rk_solve_async(rk_chain *c, int32_t M, void *d_workspace, size_t ws_bytes, v
     if (rc != RK_OK) return rc;
     DeviceScope ds(c);
     if (!ds.ok) return RK_E_DEVICE;
+    // Inside a capture of the caller's stream nothing may allocate, upload or wait: the
+    // chain must be set up by an earlier solve, and the tables are the caller's.
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (stream && hipStreamIsCapturing(static_cast<hipStream_t>(stream), &cs) != hipSuccess) return RK_E_DEVICE;
+    if (cs != hipStreamCaptureStatusNone) {
+        if (!c->d_chain || c->run_prune != c->prune || !d_workspace || c->prof.on) return RK_E_INVAL;
+        if (ws_bytes < need) return RK_E_NOMEM;
+        return fill(c, M, g, static_cast<int32_t *>(d_workspace), static_cast<hipStream_t>(stream), true);
+    }
     if ((rc = ensure_device(c)) != RK_OK) return rc;
     if (c->queued) HIPCHK(hipEventSynchronize(c->ev_fill1));  // previous fill may still read its table
     int32_t *tab;

@@ -375,3 +375,43 @@ def test_longest_chain():
         assert ops[nfwd][0] == rk.RK_BWD
     finally:
         s.close()
+
+
+def test_fill_inside_a_torch_graph_capture():
+    """The caller captures rk_solve_async into its own graph (torch.cuda.graph) after one eager
+    solve set the chain up.  Each replay refills the table from scratch: between replays the
+    workspace is overwritten with zeros and other eager work runs, and every replay's answer,
+    table and schedule must still match the oracle."""
+    import torch
+    ch = make_config_chain(1)
+    sol = oracle.solve(ch)
+    o_opt, o_arg = sol.rows()
+    exp = oracle.schedule(sol)
+    s = rk.Solver(ch)
+    try:
+        nbytes = s.workspace_bytes(ch.M)
+        ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+        st = torch.cuda.Stream()
+        s.solve_async(ch.M, ws.data_ptr(), nbytes, st.cuda_stream)  # eager: uploads the chain
+        assert s.result() == sol.answer
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=st):
+            s.solve_async(ch.M, ws.data_ptr(), nbytes, st.cuda_stream)
+        other = torch.randn(1 << 20, device="cuda:0")
+        for rep in range(3):
+            ws.zero_()
+            other.mul_(1.5)
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            say(f"  replay {rep}")
+            assert s.result() == sol.answer
+            opt, arg = s.rows(want_arg=rep == 0)
+            assert np.array_equal(opt, o_opt), rep
+            if rep == 0:
+                assert np.array_equal(arg, o_arg)
+            ops, nfwd = s.schedule()
+            assert np.array_equal(ops, exp[0]) and nfwd == exp[1]
+    finally:
+        s.close()
