@@ -74,7 +74,7 @@ struct DevChain {
 };
 
 // Largest case-1 shift that the finalize stages in LDS (larger ones read global memory).
-constexpr int32_t HMAX = 1024;
+constexpr int32_t HMAX = 256;
 
 struct Tables {
     int32_t *opt;

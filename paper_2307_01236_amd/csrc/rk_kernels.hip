@@ -511,15 +511,15 @@ __global__ __launch_bounds__(256) void k_mid(DevChain ch, Tables tb, int32_t tau
 // partial minimum the splits they did not cover (max(i-1-s, t-i) >= D, D = d rounded down
 // to a multiple of MIDMIN) and case 1 (Eq. fe), clamps, writes Opt
 // and the row's left operand ap(s, t+1) for the spans that will split after t.
-// A workgroup covers FC = 512 budgets of one cell: wave w the 128 columns from
-// mbase + 128 w, lane l the columns l and l + 64 of those, so every scalar address serves
-// two coalesced loads.  Splits go in batches of FB with all loads
-// of a batch issued before any is used; the row pointers of a split range advance
-// incrementally.  Case 1 reads one row, Opt(s+1, t, .), at K shifts: the workgroup stages
-// the columns it needs in LDS once (when the largest shift is at most HMAX), loading them
-// together with the first splits.
+// A workgroup is one wavefront covering FC = 128 budgets of one cell: lane l the columns
+// mbase + l and mbase + l + 64, so every scalar address serves two coalesced loads (single
+// waves of 128 columns beat four-wave groups of 512 and single waves of 64 or 256).
+// Splits go in batches of FB with all loads of a batch issued before any is used; the row
+// pointers of a split range advance incrementally.  Case 1 reads one row, Opt(s+1, t, .),
+// at K shifts: the wave stages the columns it needs in LDS once (when the largest shift is
+// at most HMAX), loading them together with the first splits.
 // ---------------------------------------------------------------------------------------
-constexpr int32_t FC = 512;
+constexpr int32_t FC = 128, FT = 64;  // budgets and threads per workgroup
 
 // load at a byte offset from a wave-uniform base (one scalar base + one 32-bit lane offset)
 __device__ inline int32_t ldb(const int32_t *base, uint32_t byte_off)
@@ -535,9 +535,9 @@ __device__ inline int32_t ldrow(const int32_t *base, uint32_t pitch, uint32_t by
     return __builtin_amdgcn_raw_buffer_load_b32(r, (int)byte_off, 0, 0);
 }
 
-__global__ __launch_bounds__(256) void k_finalize(DevChain ch, Tables tb, int32_t d)
+__global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t d)
 {
-    constexpr int32_t FB = 8, NC = FC / 256, NST = (HMAX + FC) / 256;
+    constexpr int32_t FB = 8, NC = FC / FT, NST = (HMAX + FC) / FT;
     __shared__ int32_t seg[HMAX + FC];
     const int32_t L = ch.L, K = ch.K, W = tb.W;
     const uint32_t n_mc = (uint32_t)(max(W, tb.padl) + FC - 1) / FC;
@@ -562,7 +562,7 @@ __global__ __launch_bounds__(256) void k_finalize(DevChain ch, Tables tb, int32_
     if (staged) {
 #pragma unroll
         for (int k = 0; k < NST; ++k) {
-            const int32_t q = (int32_t)threadIdx.x + 256 * k, c = mbase - H + q;
+            const int32_t q = (int32_t)threadIdx.x + FT * k, c = mbase - H + q;
             stv[k] = q < H + FC && c >= -padl ? rest[c] : DINF;
         }
     }
@@ -627,7 +627,7 @@ __global__ __launch_bounds__(256) void k_finalize(DevChain ch, Tables tb, int32_
     } else if (staged) {
 #pragma unroll
         for (int k = 0; k < NST; ++k) {
-            const int32_t q = (int32_t)threadIdx.x + 256 * k;
+            const int32_t q = (int32_t)threadIdx.x + FT * k;
             if (q < H + FC) seg[q] = stv[k];
         }
         __syncthreads();
@@ -770,7 +770,7 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
             if ((e = launch_mid<8>(ch, tb, stream, d, &n, prof)) != hipSuccess) return e;
         }
         if ((e = prof->before(KFILL_FINALIZE)) != hipSuccess) return e;
-        hipLaunchKernelGGL(k_finalize, dim3(fin_x * (ch.L - d)), dim3(256), 0, stream, ch, tb, d);
+        hipLaunchKernelGGL(k_finalize, dim3(fin_x * (ch.L - d)), dim3(FT), 0, stream, ch, tb, d);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if ((e = prof->after()) != hipSuccess) return e;
         ++n;

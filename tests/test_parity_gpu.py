@@ -415,3 +415,11 @@ def test_fill_inside_a_torch_graph_capture():
             assert np.array_equal(ops, exp[0]) and nfwd == exp[1]
     finally:
         s.close()
+
+
+def test_option_sizes_beyond_the_staged_halo():
+    """Options that keep up to 700 slots: case 1's shift exceeds the 256 columns the finalize
+    stages in LDS, so it reads the shifted row from global memory.  Full-table parity."""
+    ch = make_random_chain(4242, 40, 4, xmax=40, amax=700, tmax=60, tmin=0)
+    assert int(ch.mem.max()) + int(ch.x.max()) > 256
+    full_parity(ch, 3000)
