@@ -332,7 +332,7 @@ constexpr int mid_rows() { return 4; }
 
 template <int WD, bool GA, bool LO0>
 __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t tau, int32_t accumulate,
-                                int32_t wave, int32_t g)
+                                int32_t g)
 {
     constexpr int R = mid_rows<WD>(), NS = WD + R - 1, NJ = R + WD - 1;
     static_assert(WD == 8 || WD == 16, "widths 8 and 16");
@@ -416,9 +416,9 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
                 }
             }
     };
-    // The splits in the order u = (p + DL) mod NS, p = 0, 1, ...: the waves of a group (G
-    // consecutive tiles, R rows or ends apart) rotate by R (G - 1 - w) so that they all
-    // start at the same split i; their ranges differ by a shift only, so they keep visiting
+    // The splits in the order u = (p + DL) mod NS, p = 0, 1, ...: the tiles of a group (G
+    // consecutive tiles, R rows or ends apart; tile g is member w = g mod G) rotate by
+    // R (G - 1 - w) so that they all start at the same split i; their ranges differ by a shift only, so they keep visiting
     // equal splits together (also after the wrap) and share their operand rows in L2.
     auto run = [&](auto dc) {
         constexpr int DL = decltype(dc)::value;
@@ -444,9 +444,9 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
             __builtin_amdgcn_sched_barrier(0);
         });
     };
-    constexpr int G = WD == 16 ? 4 : 2;  // waves whose split ranges all share a split
+    constexpr int G = WD == 16 ? 4 : 2;  // tiles whose split ranges all share a split
     static_assert(R * (G - 1) < NS, "a group's ranges overlap");
-    const int32_t wg = wave % G;
+    const int32_t wg = g % G;
     if constexpr (G == 4) {
         if (wg == 0) run(std::integral_constant<int, 3 * R>{});
         else if (wg == 1) run(std::integral_constant<int, 2 * R>{});
@@ -491,19 +491,20 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
 
 
 
-// One launch per level: group A tiles first, then group B (both fold into the partials
-// with atomic min, so they need no order); with lo == 0 only group A, which stores.
+// One launch per level, one wavefront per workgroup and tile (single waves measured a
+// little faster than four-wave groups): group A tiles first, then group B (both fold into
+// the partials with atomic min, so they need no order); with lo == 0 only group A, which
+// stores.  Consecutive tiles run on one XCD.
 template <int WD, bool LO0>
-__global__ __launch_bounds__(256) void k_mid(DevChain ch, Tables tb, int32_t tau, int32_t accumulate)
+__global__ __launch_bounds__(64) void k_mid(DevChain ch, Tables tb, int32_t tau, int32_t accumulate)
 {
     constexpr int R = mid_rows<WD>();
-    const int32_t wave = __builtin_amdgcn_readfirstlane((int32_t)(threadIdx.x >> 6));
     const int32_t per_group = (ch.L - tau + R - 1) / R * ((tb.W + 63) / 64);
-    const int32_t g = (int32_t)xcd_tile(blockIdx.x, gridDim.x) * 4 + wave;
+    const int32_t g = (int32_t)xcd_tile(blockIdx.x, gridDim.x);
     if (g < per_group)
-        mid_tile<WD, true, LO0>(ch, tb, tau, accumulate, wave, g);
+        mid_tile<WD, true, LO0>(ch, tb, tau, accumulate, g);
     else if (!LO0 && g < 2 * per_group)
-        mid_tile<WD, false, false>(ch, tb, tau, accumulate, wave, g - per_group);
+        mid_tile<WD, false, false>(ch, tb, tau, accumulate, g - per_group);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -720,12 +721,12 @@ static hipError_t launch_mid(const DevChain &ch, const Tables &tb, hipStream_t s
     const int32_t lo = d - WD;
     constexpr int R = mid_rows<WD>();
     const int32_t n_blk = (ch.L - d + R - 1) / R, n_mc = (tb.W + 63) / 64;
-    const dim3 grid(((lo == 0 ? 1 : 2) * n_blk * n_mc + 3) / 4);
+    const dim3 grid((lo == 0 ? 1 : 2) * n_blk * n_mc);
     if ((e = prof->before(KFILL_MID)) != hipSuccess) return e;
     if (lo == 0)
-        hipLaunchKernelGGL((k_mid<WD, true>), grid, dim3(256), 0, stream, ch, tb, d, 0);
+        hipLaunchKernelGGL((k_mid<WD, true>), grid, dim3(64), 0, stream, ch, tb, d, 0);
     else
-        hipLaunchKernelGGL((k_mid<WD, false>), grid, dim3(256), 0, stream, ch, tb, d, 1);
+        hipLaunchKernelGGL((k_mid<WD, false>), grid, dim3(64), 0, stream, ch, tb, d, 1);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = prof->after()) != hipSuccess) return e;
     ++*n;
