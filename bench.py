@@ -10,8 +10,8 @@ the solve runs on a torch stream.
 Prints one JSON line on stdout.  ``value`` is DP relaxations per second of
 the whole step (relaxations = candidate evaluations of the recurrence,
 (M+1) * sum_d (L-d)(K+d)).  ``roofline`` reports the dominant fill kernel (the
-kind with the most device time, from per-launch HIP events on the solve's
-stream) against the roof that binds it: HBM bandwidth for its compulsory table
+kind with the most device time, from HIP events the runtime records with each
+dispatch on the solve's stream) against the roof that binds it: HBM bandwidth for its compulsory table
 traffic (every row a launch reads counted once, plus the rows it writes) or the
 VALU integer peak for its relaxations (an add and a min each), whichever
 fraction is higher; the other one is reported beside it; both are also priced
@@ -209,8 +209,8 @@ def main():
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, fill median {statistics.median(fill_ms):.3f} ms")
 
-    # the same steps again with every kernel launch bracketed by HIP events on the solve's
-    # stream (launched one by one): per-kernel durations for the roofline
+    # the same steps again with the kernels launched one by one, each dispatch recording a
+    # pair of HIP events at the kernel's start and end: per-kernel durations for the roofline
     s.set_profiling(True)
     kern = {}
     for i in range(args.steps):

@@ -164,10 +164,10 @@ int rk_tradeoff_curve(rk_chain *c, int32_t *times, int64_t n);
 int rk_last_fill_ms(rk_chain *c, float *ms, int32_t *launches);
 
 /*
- * Kernel-level timing (for benchmarks; off by default).  While enabled, every
- * kernel the fill launches is bracketed by a pair of HIP events on the solve's
- * stream, and the fill launches its kernels one by one instead of replaying a
- * graph.  rk_fill_kernel_stats then reports, for kernel kind `kind`
+ * Kernel-level timing (for benchmarks; off by default).  While enabled, the fill
+ * launches its kernels one by one instead of replaying a graph, and the runtime
+ * records a pair of HIP events with every dispatch, at the kernel's start and end
+ * (hipExtLaunchKernelGGL), so a launch's time is the kernel's own.  rk_fill_kernel_stats then reports, for kernel kind `kind`
  * (0 <= kind < *n_kinds), its name as a profiler shows it, the number of its
  * launches in the last solve, their summed device time in milliseconds, the
  * number of candidate evaluations of the recurrence (relaxations, counting

@@ -103,8 +103,8 @@ struct Profiler {
     int32_t n = 0;                   // launches bracketed in the current solve
     int64_t work[8] = {};            // relaxations per kernel kind in the current solve
     int64_t bytes[8] = {};           // compulsory table traffic per kernel kind
-    hipError_t before(int32_t kind);
-    hipError_t after();
+    // two events from the pool for the next launch, which is of kind `kind`
+    hipError_t slot(int32_t kind, hipEvent_t *start, hipEvent_t *stop);
     void reset(hipStream_t s)
     {
         stream = s;

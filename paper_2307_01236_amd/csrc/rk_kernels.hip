@@ -13,15 +13,16 @@
 // attains Opt(s,t,m)), so the fill keeps no argmin bookkeeping.
 #include "rk_internal.h"
 
+#include <hip/hip_ext.h>
+
 #include <type_traits>
 
 namespace rk {
 
 const char *const kFillKernelNames[KFILL_NKINDS] = {"k_product", "k_mid", "k_finalize", "k_init_inf_rows"};
 
-hipError_t Profiler::before(int32_t kind)
+hipError_t Profiler::slot(int32_t kind, hipEvent_t *start, hipEvent_t *stop)
 {
-    if (!on) return hipSuccess;
     while ((int32_t)events.size() < 2 * (n + 1)) {
         hipEvent_t e;
         hipError_t err = hipEventCreate(&e);
@@ -29,15 +30,28 @@ hipError_t Profiler::before(int32_t kind)
         events.push_back(e);
     }
     kinds.push_back(kind);
-    return hipEventRecord(events[2 * n], stream);
+    *start = events[2 * n];
+    *stop = events[2 * n + 1];
+    ++n;
+    return hipSuccess;
 }
 
-hipError_t Profiler::after()
+// Launch one fill kernel.  With profiling on, the runtime records a pair of events with the
+// dispatch itself (hipExtLaunchKernelGGL), at the kernel's start and end, so the elapsed
+// time is the kernel's own, without the gaps between launches.
+template <typename K, typename... Args>
+static hipError_t launch(Profiler *prof, int32_t kind, K kernel, dim3 grid, dim3 block, hipStream_t stream,
+                         Args... args)
 {
-    if (!on) return hipSuccess;
-    hipError_t err = hipEventRecord(events[2 * n + 1], stream);
-    ++n;
-    return err;
+    if (!prof->on) {
+        hipLaunchKernelGGL(kernel, grid, block, 0, stream, args...);
+        return hipGetLastError();
+    }
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    const hipError_t e = prof->slot(kind, &e0, &e1);
+    if (e != hipSuccess) return e;
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, e0, e1, 0, args...);
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------------------
@@ -722,13 +736,9 @@ static hipError_t launch_mid(const DevChain &ch, const Tables &tb, hipStream_t s
     constexpr int R = mid_rows<WD>();
     const int32_t n_blk = (ch.L - d + R - 1) / R, n_mc = (tb.W + 63) / 64;
     const dim3 grid((lo == 0 ? 1 : 2) * n_blk * n_mc);
-    if ((e = prof->before(KFILL_MID)) != hipSuccess) return e;
-    if (lo == 0)
-        hipLaunchKernelGGL((k_mid<WD, true>), grid, dim3(64), 0, stream, ch, tb, d, 0);
-    else
-        hipLaunchKernelGGL((k_mid<WD, false>), grid, dim3(64), 0, stream, ch, tb, d, 1);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = prof->after()) != hipSuccess) return e;
+    e = lo == 0 ? launch(prof, KFILL_MID, k_mid<WD, true>, grid, dim3(64), stream, ch, tb, d, 0)
+                : launch(prof, KFILL_MID, k_mid<WD, false>, grid, dim3(64), stream, ch, tb, d, 1);
+    if (e != hipSuccess) return e;
     ++*n;
     prof->work[KFILL_MID] += lo == 0 ? product_work(ch.L, tb.W, d, WD, 0, WD, 0, WD)
                                      : product_work(ch.L, tb.W, d, WD, lo, d, 0, d) +
@@ -747,21 +757,17 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
     static_assert(BAND == 32 && MIDMIN == 8, "the launch sequence below is written for these");
     hipError_t e;
     int32_t n = 0;
-    if ((e = prof->before(KFILL_INIT)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_init_inf_rows, dim3((tb.stride + 255) / 256, 2 * (2 * SLACK + 1)), dim3(256), 0,
-                       stream, tb);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = prof->after()) != hipSuccess) return e;
+    e = launch(prof, KFILL_INIT, k_init_inf_rows, dim3((tb.stride + 255) / 256, 2 * (2 * SLACK + 1)), dim3(256),
+               stream, tb);
+    if (e != hipSuccess) return e;
     ++n;
     const int32_t fin_x = (max(tb.W, tb.padl) + FC - 1) / FC;
     for (int32_t d = 0; d < ch.L; ++d) {
         if (d > 0 && d % BAND == 0) {
             constexpr int SR = 4, TW = 16, TH = 2, NW = 4, SW = SR * NW / TH;  // product tile
             const dim3 grid(((tb.W + 63) / 64) * ((ch.L - d + SW - 1) / SW));
-            if ((e = prof->before(KFILL_PRODUCT)) != hipSuccess) return e;
-            hipLaunchKernelGGL((k_product<SR, TW, TH, NW>), grid, dim3(NW * 64), 0, stream, ch, tb, d);
-            if ((e = hipGetLastError()) != hipSuccess) return e;
-            if ((e = prof->after()) != hipSuccess) return e;
+            e = launch(prof, KFILL_PRODUCT, k_product<SR, TW, TH, NW>, grid, dim3(NW * 64), stream, ch, tb, d);
+            if (e != hipSuccess) return e;
             ++n;
             prof->work[KFILL_PRODUCT] += product_work(ch.L, tb.W, d, BAND, 0, d, 0, d);
             prof->bytes[KFILL_PRODUCT] += product_bytes(ch.L, tb.W, d, BAND, 0, d, 0, d, false);
@@ -770,10 +776,8 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
         } else if (d % 8 == 0 && d > 0) {
             if ((e = launch_mid<8>(ch, tb, stream, d, &n, prof)) != hipSuccess) return e;
         }
-        if ((e = prof->before(KFILL_FINALIZE)) != hipSuccess) return e;
-        hipLaunchKernelGGL(k_finalize, dim3(fin_x * (ch.L - d)), dim3(FT), 0, stream, ch, tb, d);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        if ((e = prof->after()) != hipSuccess) return e;
+        e = launch(prof, KFILL_FINALIZE, k_finalize, dim3(fin_x * (ch.L - d)), dim3(FT), stream, ch, tb, d);
+        if (e != hipSuccess) return e;
         ++n;
         const int32_t D = (d / MIDMIN) * MIDMIN, near = D > 0 ? 2 * (d - D) : d;
         prof->work[KFILL_FINALIZE] += (int64_t)(ch.L - d) * (near + ch.K) * tb.W;
