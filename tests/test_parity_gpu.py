@@ -423,3 +423,40 @@ def test_option_sizes_beyond_the_staged_halo():
     ch = make_random_chain(4242, 40, 4, xmax=40, amax=700, tmax=60, tmin=0)
     assert int(ch.mem.max()) + int(ch.x.max()) > 256
     full_parity(ch, 3000)
+
+
+@pytest.mark.parametrize("idx", range(8))
+def test_medium_random_chains_sampled(idx):
+    """Random chains of 110-260 blocks (several bands, ragged band and column tails), 1-24
+    options, budgets 300-2500: exact parity on three sampled sub-chains, and on the whole
+    table the infeasibility pattern, monotonicity in m and a schedule that replays at the
+    answer."""
+    rng = np.random.default_rng(4100 + idx)
+    L = int(rng.integers(110, 261))
+    K = int(rng.integers(1, 25))
+    ch = make_random_chain(4100 + idx, L, K, xmax=int(rng.integers(1, 30)), amax=int(rng.integers(1, 80)),
+                           tmax=int(rng.integers(0, 30)), tmin=0, small_times=idx % 2 == 0,
+                           allow_zero=idx % 3 == 0)
+    M = int(rng.integers(300, 2501))
+    say(f"  medium chain L={L} K={K} M={M}")
+    s = rk.Solver(ch)
+    try:
+        ans = s.solve(M)
+        for s0, n in ((0, 16), (int(rng.integers(1, L - 16)), 16), (L - 16, 16)):
+            sub_rows_parity(s, ch, s0, n)
+        mf = oracle.min_feasible(ch)
+        cells = oracle.cell_index(L)
+        m = np.arange(M + 1)
+        for _ in range(30):
+            a = int(rng.integers(0, L))
+            b = int(rng.integers(a, L))
+            row, _ = s.row(a, b, want_arg=False)
+            assert np.array_equal(row != INF, m >= mf[cells[a, b]]), (a, b)
+            r64 = row.astype(np.int64)
+            assert (r64[1:] <= r64[:-1]).all(), (a, b)
+        if ans != INF:
+            ops, nfwd = s.schedule()
+            ok, tm, pk, bad = oracle.simulate(ch, ops)
+            assert ok and tm == ans and pk <= M, (ok, tm, ans, pk, bad)
+    finally:
+        s.close()
