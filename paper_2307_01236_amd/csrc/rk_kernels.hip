@@ -191,10 +191,19 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
 
     // fetch(ic) issues the loads of chunk ic; their values are first used one chunk later
     uint32_t qv[CI][JW], av[CI][SR];
+    // Bases of the chunk being fetched: its right-operand block starts one row before
+    // (ic, t0), its left-operand block at row (s0, ic - 1).  They advance with ic (row (i+1, t)
+    // is L-1-i rows after (i, t), within the workspace guard's 2 GiB) and are recomputed
+    // where the chunk order wraps around.
+    const int32_t *qcur = nullptr, *acur = nullptr;
+    auto seek = [&](int32_t ic) {
+        qcur = tb.opt + (row_of(L, ic, t0) - 1) * stride;
+        acur = tb.ap + row_of(L, s0, ic - 1) * stride;
+    };
     auto fetch = [&](int32_t ic) {
         // right operands from one row before (ic, t0): split i's rows start rel(i) rows on,
         // shifted left by min(x_i, padl) columns (a larger x_i reads only the left pad)
-        const int32_t *const qb = tb.opt + (row_of(L, ic, t0) - 1) * stride;
+        const int32_t *const qb = qcur;
         const __amdgpu_buffer_rsrc_t rq = block_rsrc(qb, opt_end);
         // Operands that are not used are not read: a staged row whose right span
         // t0 + jj*NW + wave - ic - ii is outside [0, tau), or a left operand whose span
@@ -221,7 +230,7 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
             rel += (uint32_t)max(L - 1 - i, 0);
         }
         // left operands: rows (s0 + r, ic + ii - 1), consecutive in ii
-        const int32_t *const ab = tb.ap + row_of(L, s0, ic - 1) * stride;
+        const int32_t *const ab = acur;
         const __amdgpu_buffer_rsrc_t ra = block_rsrc(ab, ap_end);
         const int32_t a0 = ic - 1 - s0;
         if (a0 - (SR - 1) >= 0 && a0 + CI - 1 < tau) {
@@ -255,6 +264,7 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
         return c + CI < anchor ? c + CI : DONE;
     };
 
+    seek(anchor);
     fetch(anchor);
     for (int32_t ic = anchor, buf = 0; ic != DONE; buf ^= 1) {
         const int32_t inext = next_chunk(ic);
@@ -289,7 +299,18 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
                 for (int r = 0; r < SR; ++r) a[ii][r] = r - ii > alim ? av[ii][r] : DINF;
         }
         __syncthreads();
-        if (inext != DONE) fetch(inext);  // in flight while this chunk is relaxed
+        if (inext != DONE) {  // in flight while this chunk is relaxed
+            if (inext == ic + CI) {
+                int32_t rows = 0;
+#pragma unroll
+                for (int ii = 0; ii < CI; ++ii) rows += L - 1 - (ic + ii);
+                qcur = (const int32_t *)((const char *)qcur + (int64_t)rows * pitch);
+                acur = (const int32_t *)((const char *)acur + (int64_t)CI * pitch);
+            } else {
+                seek(inext);
+            }
+            fetch(inext);
+        }
         // acc(s0+r, s0+r+tau+k) = min(acc, ap(s0+r, i) + Opt(i, s0+r+tau+k, m - x_i)), two splits per min
 #pragma unroll
         for (int ii = 0; ii < CI; ii += 2)
