@@ -926,7 +926,6 @@ __global__ __launch_bounds__(64) void k_backtrace(DevChain ch, Tables tb, int32_
     // The cell being resolved stays in registers; the stack holds what comes after it.
     int32_t s = 0, t = L - 1, m = m_top;
     bool have = true;
-    constexpr int NB = 8;  // split candidates per lane per round of loads
     for (;;) {
         if (!have) {
             if (sp == 0) break;
@@ -948,6 +947,10 @@ __global__ __launch_bounds__(64) void k_backtrace(DevChain ch, Tables tb, int32_
         const uint32_t ustride = (uint32_t)stride;
         const int32_t *const ap_s = tb.ap + (uint64_t)row32(s, s) * ustride + padl + m;
         const int32_t rest_row = row32(min(s + 1, t), t);
+        // NB split candidates per lane and round of loads: as many as the cell has splits
+        // (up to 8 per lane), so short spans do not pay for the longest ones
+        auto cell = [&](auto nbc) {
+        constexpr int NB = decltype(nbc)::value;
         const int32_t rounds = max((d + 64 * NB - 1) / (64 * NB), (K + 63) / 64);
         for (int32_t r = 0; r < rounds; ++r) {
             // the option's xbar first: when it comes from global memory, the rest's address
@@ -974,6 +977,11 @@ __global__ __launch_bounds__(64) void k_backtrace(DevChain ch, Tables tb, int32_
             }
             take(o < K && m >= need, (uint32_t)c1 + (uint32_t)rest, (uint32_t)(L + o));
         }
+        };
+        if (d <= 64) cell(std::integral_constant<int, 1>{});
+        else if (d <= 128) cell(std::integral_constant<int, 2>{});
+        else if (d <= 256) cell(std::integral_constant<int, 4>{});
+        else cell(std::integral_constant<int, 8>{});
         const uint32_t bc = (uint32_t)(best >> 32), bk = (uint32_t)best;
         const uint32_t cost = wave_min_u32(bc);
         const uint32_t code = wave_min_u32(bc == cost ? bk : ~0u);
