@@ -527,19 +527,28 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
 
 
 // One launch per level, one wavefront per workgroup and tile (single waves measured a
-// little faster than four-wave groups): group A tiles first, then group B (both fold into
-// the partials with atomic min, so they need no order); with lo == 0 only group A, which
-// stores.  Consecutive tiles run on one XCD.
+// little faster than four-wave groups).  Groups A and B fold into the partials with atomic
+// min, so they need no order; with lo == 0 only group A, which stores.  Tiles go column
+// chunk by column chunk (group A's row blocks, then group B's), and consecutive tiles run
+// on one XCD: each XCD keeps the same range of columns as in the finalize launches, whose
+// recent rows the mids read.
 template <int WD, bool LO0>
 __global__ __launch_bounds__(64) void k_mid(DevChain ch, Tables tb, int32_t tau, int32_t accumulate)
 {
     constexpr int R = mid_rows<WD>();
-    const int32_t per_group = (ch.L - tau + R - 1) / R * ((tb.W + 63) / 64);
+    const int32_t n_blk = (ch.L - tau + R - 1) / R;
+    const int32_t per_group = n_blk * ((tb.W + 63) / 64);
     const int32_t g = (int32_t)xcd_tile(blockIdx.x, gridDim.x);
-    if (g < per_group)
-        mid_tile<WD, true, LO0>(ch, tb, tau, accumulate, g);
-    else if (!LO0 && g < 2 * per_group)
-        mid_tile<WD, false, false>(ch, tb, tau, accumulate, g - per_group);
+    if (LO0) {
+        if (g < per_group) mid_tile<WD, true, LO0>(ch, tb, tau, accumulate, g);
+    } else {
+        // column chunk mc, then group A's n_blk tiles and group B's; gi indexes the group
+        const int32_t mc = g / (2 * n_blk), rem = g % (2 * n_blk), gi = mc * n_blk + rem % n_blk;
+        if (mc * n_blk < per_group) {
+            if (rem < n_blk) mid_tile<WD, true, false>(ch, tb, tau, accumulate, gi);
+            else mid_tile<WD, false, false>(ch, tb, tau, accumulate, gi);
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------------------
