@@ -460,3 +460,11 @@ def test_medium_random_chains_sampled(idx):
             assert ok and tm == ans and pk <= M, (ok, tm, ans, pk, bad)
     finally:
         s.close()
+
+
+def test_wide_budget():
+    """200 001 budget columns on a short chain with large sizes: a left pad of ~2000 columns,
+    1 563 column chunks per cell in the finalize and shifts far beyond its staged halo.
+    Full-table parity."""
+    ch = make_random_chain(777, 12, 3, xmax=2000, amax=9000, tmax=3000, tmin=0)
+    full_parity(ch, 200000)
