@@ -8,8 +8,9 @@
 // data-parallel step over (s, m); lanes run along m, so every table read of a
 // wave is one contiguous 256-byte segment (shifted by a per-block constant).
 //
-// Only Opt is stored.  Which choice realises a minimum is recomputed from the
-// finished table where it is needed (Alg. 3 does the same: it asks which case
+// Only values are stored: Opt and ap, the left operand of Eq. fn with the sweep's
+// time and validity folded in.  Which choice realises a minimum is recomputed from
+// the finished table where it is needed (Alg. 3 does the same: it asks which case
 // attains Opt(s,t,m)), so the fill keeps no argmin bookkeeping.
 #include "rk_internal.h"
 
