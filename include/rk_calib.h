@@ -3,7 +3,7 @@
  * solver runs on, for pricing its kernels against what the chip sustains next to
  * the nominal peaks.  Not part of the solver; the benchmark calls it.
  *
- * Both calls run on the current HIP device, on a stream of their own, and wait
+ * The calls run on the current HIP device, on a stream of their own, and wait
  * for their kernels.  Return 0 on success, -1 (RKC_E_INVAL) for a bad argument,
  * -3 (RKC_E_NOMEM) when device memory cannot be allocated, -4 (RKC_E_DEVICE) for
  * any other HIP error.  Results are host values the caller owns.
@@ -36,6 +36,15 @@ int rkc_valu_int32_rate(int32_t iters, double *ops_per_s);
  * after one warm-up, per grid).  Allocates the two buffers for the call and frees them.
  */
 int rkc_copy_bandwidth(int64_t bytes, double *bytes_per_s);
+
+/*
+ * Sustained device-memory read bandwidth: a kernel with 16-byte loads reads `bytes` (a
+ * positive multiple of 16, at most 2^36) of one device buffer and writes nothing back,
+ * with 2, 4, 8 and 16 workgroups of 256 lanes per compute unit; *bytes_per_s receives
+ * bytes read per second of the fastest (best of three timed reads after one warm-up,
+ * per grid).  Allocates the buffer for the call and frees it.
+ */
+int rkc_read_bandwidth(int64_t bytes, double *bytes_per_s);
 
 #ifdef __cplusplus
 }

@@ -1,6 +1,6 @@
 """Python binding of librkcalib (include/rk_calib.h): argument marshalling only.
 
-Measured ceilings of the GPU (int32 VALU rate, copy bandwidth) for the
+Measured ceilings of the GPU (int32 VALU rate, copy and read bandwidth) for the
 benchmark's roofline; the kernels run in the HIP library.
 """
 from __future__ import annotations
@@ -10,7 +10,7 @@ import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "librkcalib.so")
-EXPORTS = ("rkc_valu_int32_rate", "rkc_copy_bandwidth")
+EXPORTS = ("rkc_valu_int32_rate", "rkc_copy_bandwidth", "rkc_read_bandwidth")
 
 _lib = None
 
@@ -24,6 +24,7 @@ def load():
         lib = C.CDLL(LIB_PATH)
         lib.rkc_valu_int32_rate.argtypes = [C.c_int32, C.POINTER(C.c_double)]
         lib.rkc_copy_bandwidth.argtypes = [C.c_int64, C.POINTER(C.c_double)]
+        lib.rkc_read_bandwidth.argtypes = [C.c_int64, C.POINTER(C.c_double)]
         for n in EXPORTS:
             getattr(lib, n).restype = C.c_int
         _lib = lib
@@ -46,3 +47,8 @@ def valu_int32_rate(iters: int = 1 << 14) -> float:
 def copy_bandwidth(nbytes: int = 1 << 30) -> float:
     """Sustained device copy bandwidth, bytes read plus written per second."""
     return _call("rkc_copy_bandwidth", int(nbytes))
+
+
+def read_bandwidth(nbytes: int = 1 << 30) -> float:
+    """Sustained device read bandwidth, bytes read per second."""
+    return _call("rkc_read_bandwidth", int(nbytes))

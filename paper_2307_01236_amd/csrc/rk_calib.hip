@@ -36,6 +36,19 @@ __global__ __launch_bounds__(256) void k_copy(const uint4 *__restrict__ src, uin
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += step) dst[i] = src[i];
 }
 
+// A streaming read: every lane folds the 16-byte words it loads into one value, written
+// only if it equals a value it practically never takes (so the loads stay).
+__global__ __launch_bounds__(256) void k_read(const uint4 *__restrict__ src, uint32_t *out, int64_t n)
+{
+    const int64_t step = (int64_t)gridDim.x * blockDim.x;
+    uint32_t acc = 0;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += step) {
+        const uint4 v = src[i];
+        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+    if (acc == 0x9e3779b9u) out[blockIdx.x] = acc;
+}
+
 // Best of three timed runs of `launch` after one warm-up, in seconds.
 template <class F>
 int best_of_three(hipStream_t st, F launch, double *sec)
@@ -112,5 +125,42 @@ extern "C" int rkc_copy_bandwidth(int64_t bytes, double *bytes_per_s)
     (void)hipFree(dst);
     if (rc != RKC_OK) return rc;
     *bytes_per_s = 2.0 * (double)bytes / sec;
+    return RKC_OK;
+}
+
+extern "C" int rkc_read_bandwidth(int64_t bytes, double *bytes_per_s)
+{
+    if (!bytes_per_s || bytes <= 0 || bytes % 16 || bytes > (int64_t(1) << 36)) return RKC_E_INVAL;
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+        return RKC_E_DEVICE;
+    constexpr int MAX_PER_CU = 16;
+    void *src = nullptr;
+    uint32_t *out = nullptr;
+    if (hipMalloc(&src, (size_t)bytes) != hipSuccess) return RKC_E_NOMEM;
+    if (hipMalloc(&out, (size_t)cus * MAX_PER_CU * sizeof(uint32_t)) != hipSuccess) {
+        (void)hipFree(src);
+        return RKC_E_NOMEM;
+    }
+    hipStream_t st = nullptr;
+    int rc = hipStreamCreate(&st) == hipSuccess && hipMemsetAsync(src, 1, (size_t)bytes, st) == hipSuccess
+                 ? RKC_OK
+                 : RKC_E_DEVICE;
+    double sec = 1e30;
+    const int64_t n = bytes / 16;
+    for (int per_cu : {2, 4, 8, MAX_PER_CU}) {
+        if (rc != RKC_OK) break;
+        double t = 0.0;
+        rc = best_of_three(st, [&] {
+            hipLaunchKernelGGL(k_read, dim3(cus * per_cu), dim3(256), 0, st, (const uint4 *)src, out, n);
+        }, &t);
+        sec = std::min(sec, t);
+    }
+    if (st) (void)hipStreamDestroy(st);
+    (void)hipFree(src);
+    (void)hipFree(out);
+    if (rc != RKC_OK) return rc;
+    *bytes_per_s = (double)bytes / sec;
     return RKC_OK;
 }

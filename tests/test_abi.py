@@ -42,6 +42,9 @@ def test_calibration_library_exports():
     assert lib.rkc_valu_int32_rate(0, C.byref(out)) == -1
     assert lib.rkc_copy_bandwidth(17, C.byref(out)) == -1
     assert lib.rkc_copy_bandwidth(1 << 30, None) == -1
+    assert lib.rkc_read_bandwidth(17, C.byref(out)) == -1
+    assert lib.rkc_read_bandwidth(0, C.byref(out)) == -1
+    assert lib.rkc_read_bandwidth(1 << 30, None) == -1
 
 
 def test_constants_match_header():
