@@ -371,7 +371,7 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
                                 int32_t g)
 {
     constexpr int R = mid_rows<WD>(), NS = WD + R - 1, NJ = R + WD - 1;
-    static_assert(WD == 8 || WD == 16, "widths 8 and 16");
+    static_assert(WD == 4 || WD == 8 || WD == 16, "widths 4, 8 and 16");
     static_assert(GA || !LO0, "lo == 0 is group A only");
     static_assert(NJ - 1 <= OFFSET_SPAN_L && NJ + 1 <= OFFSET_SPAN_C, "operand offsets fit the workspace guard");
     const int32_t L = ch.L, W = tb.W, lo = tau - WD;
@@ -473,9 +473,11 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
                                  "v"(acc[r][4]), "v"(acc[r][5]), "v"(acc[r][6]), "v"(acc[r][7]), "v"(acc[r][8]),
                                  "v"(acc[r][9]), "v"(acc[r][10]), "v"(acc[r][11]), "v"(acc[r][12]),
                                  "v"(acc[r][13]), "v"(acc[r][14]), "v"(acc[r][15]));
-                else
+                else if constexpr (WD == 8)
                     asm volatile("" ::"v"(acc[r][0]), "v"(acc[r][1]), "v"(acc[r][2]), "v"(acc[r][3]),
                                  "v"(acc[r][4]), "v"(acc[r][5]), "v"(acc[r][6]), "v"(acc[r][7]));
+                else
+                    asm volatile("" ::"v"(acc[r][0]), "v"(acc[r][1]), "v"(acc[r][2]), "v"(acc[r][3]));
             }
             __builtin_amdgcn_sched_barrier(0);
         });
@@ -555,7 +557,7 @@ __global__ __launch_bounds__(64) void k_mid(DevChain ch, Tables tb, int32_t tau,
 // ---------------------------------------------------------------------------------------
 // Finalize one span-length diagonal d: cell (s, s+d), budgets m.  Adds to the products'
 // partial minimum the splits they did not cover (max(i-1-s, t-i) >= D, D = d rounded down
-// to a multiple of MIDMIN) and case 1 (Eq. fe), clamps, writes Opt
+// to a multiple of midmin, the narrowest mid width) and case 1 (Eq. fe), clamps, writes Opt
 // and the row's left operand ap(s, t+1) for the spans that will split after t.
 // A workgroup is one wavefront covering FC = 128 budgets of one cell: lane l the columns
 // mbase + l and mbase + l + 64, so every scalar address serves two coalesced loads (single
@@ -581,7 +583,7 @@ __device__ inline int32_t ldrow(const int32_t *base, uint32_t pitch, uint32_t by
     return __builtin_amdgcn_raw_buffer_load_b32(r, (int)byte_off, 0, 0);
 }
 
-__global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t d)
+__global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t d, int32_t midmin)
 {
     constexpr int32_t FB = 8, NC = FC / FT, NST = (HMAX + FC) / FT;
     __shared__ int32_t seg[HMAX + FC];
@@ -601,7 +603,7 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
     const uint32_t pitch = (uint32_t)stride * 4u;
     const int32_t padl = tb.padl;
     int32_t *const orow = tb.opt + row_of(L, s, t) * stride + padl;  // column 0
-    const int32_t D = (d / MIDMIN) * MIDMIN;  // the products cover splits with max(a, b) < D
+    const int32_t D = (d / midmin) * midmin;  // the products cover splits with max(a, b) < D
 
     // case-1 row, staged: column mbase - H + q at seg[q]
     const int32_t H = ch.xbar_halo;
@@ -784,13 +786,14 @@ static hipError_t launch_mid(const DevChain &ch, const Tables &tb, hipStream_t s
 }
 
 // The fill: per diagonal d, the products that complete before it (a band product every
-// BAND spans, mid products in between down to MIDMIN), then its finalize.
+// BAND spans, mid products in between down to width midmin), then its finalize.
 hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream, int32_t *launches,
                        Profiler *prof)
 {
-    static_assert(BAND == 32 && MIDMIN == 8, "the launch sequence below is written for these");
+    static_assert(BAND == 32, "the launch sequence below is written for 32-span bands");
     hipError_t e;
     int32_t n = 0;
+    const int32_t midmin = fill_midmin(ch.L, tb.W);
     e = launch(prof, KFILL_INIT, k_init_inf_rows, dim3((tb.stride + 255) / 256, 2 * (2 * SLACK + 1)), dim3(256),
                stream, tb);
     if (e != hipSuccess) return e;
@@ -809,11 +812,14 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
             if ((e = launch_mid<16>(ch, tb, stream, d, &n, prof)) != hipSuccess) return e;
         } else if (d % 8 == 0 && d > 0) {
             if ((e = launch_mid<8>(ch, tb, stream, d, &n, prof)) != hipSuccess) return e;
+        } else if (d % 4 == 0 && d > 0 && midmin == 4) {
+            if ((e = launch_mid<4>(ch, tb, stream, d, &n, prof)) != hipSuccess) return e;
         }
-        e = launch(prof, KFILL_FINALIZE, k_finalize, dim3(fin_x * (ch.L - d)), dim3(FT), stream, ch, tb, d);
+        e = launch(prof, KFILL_FINALIZE, k_finalize, dim3(fin_x * (ch.L - d)), dim3(FT), stream, ch, tb, d,
+                   midmin);
         if (e != hipSuccess) return e;
         ++n;
-        const int32_t D = (d / MIDMIN) * MIDMIN, near = D > 0 ? 2 * (d - D) : d;
+        const int32_t D = (d / midmin) * midmin, near = D > 0 ? 2 * (d - D) : d;
         prof->work[KFILL_FINALIZE] += (int64_t)(ch.L - d) * (near + ch.K) * tb.W;
         // per cell: two operand rows per split, the stored partial, the case-1 row, the Opt
         // row written; the ap row written where a later split uses it

@@ -462,6 +462,26 @@ def test_medium_random_chains_sampled(idx):
         s.close()
 
 
+@pytest.mark.parametrize("M", [24998, 25000])
+def test_mid_width_four_on_and_off(M):
+    """64 blocks at budgets either side of the table size (blocks x budget columns =
+    1.6e6) from which the fill adds mid products of width 4 and its finalize covers only the
+    splits whose longer operand spans the last 4 spans: full-table parity in both regimes."""
+    ch = make_random_chain(6464, 64, 3, xmax=50, amax=400, tmax=100, tmin=0)
+    sol = full_parity(ch, M)
+    assert sol.answer != INF
+    s = rk.Solver(ch)
+    try:
+        s.set_profiling(True)
+        s.solve(M)
+        n_mid = s.kernel_stats()["k_mid"][0]
+    finally:
+        s.close()
+    # mids of width 16 at d = 16, 48 and of width 8 at d = 8, 24, 40, 56; of width 4 at
+    # d = 4, 12, ..., 60 when blocks x budget columns reaches 1.6e6
+    assert n_mid == (14 if ch.L * (M + 1) >= 1_600_000 else 6), n_mid
+
+
 def test_wide_budget():
     """200 001 budget columns on a short chain with large sizes: a left pad of ~2000 columns,
     1 563 column chunks per cell in the finalize and shifts far beyond its staged halo.
