@@ -103,8 +103,8 @@ int geometry(const rk_chain *c, int32_t M, Geometry *g, size_t *bytes)
     g->rows = rk::n_rows(c->L) + 1;
     const int64_t elems = 2 * rk::table_rows(c->L) * (int64_t)g->stride;
     if (elems <= 0 || elems > (int64_t(1) << 40)) return RK_E_NOMEM;
-    // the band product addresses the operand rows of one chunk of splits with 32-bit byte
-    // offsets from a chunk base
+    // the products address each operand block with 32-bit byte offsets from its first row;
+    // the widest block spans OFFSET_SPAN_L (L - 1) + OFFSET_SPAN_C rows
     if ((rk::OFFSET_SPAN_L * (int64_t)c->L + rk::OFFSET_SPAN_C) * g->stride * 4 >= (int64_t(1) << 31))
         return RK_E_NOMEM;
     *bytes = (size_t)elems * sizeof(int32_t);
