@@ -22,8 +22,9 @@ share of bytes written).  ``cpu_baseline``
 times the CPU oracle (one core) on a bounded part of the same chain.  After
 the timed and profiled steps, ``tradeoff`` and ``option_pruning`` report the
 memory/time trade-off curve of the fill against Rotor's (Sec. 4) and the effect
-of option pruning on a chain with an emulated budget-grid option search
-(``--extras 0`` skips both, for profiler runs that should see one workload).
+of option pruning on a chain with an emulated budget-grid option search, and
+``other_workloads`` the fill times of the four smaller workloads (``--extras 0``
+skips all three, for profiler runs that should see one workload).
 """
 from __future__ import annotations
 
@@ -103,7 +104,8 @@ def cpu_baseline(ch, nblocks: int):
 
 
 def extras(ch, s, M):
-    """Reports beside the benchmark: the trade-off curve against Rotor's and option pruning."""
+    """Reports beside the benchmark: the trade-off curve against Rotor's, option pruning and
+    the fill of the smaller workloads."""
     from paper_2307_01236_amd import rk
     from paper_2307_01236_amd.chaingen import make_grid_chain, relaxations
 
@@ -146,7 +148,26 @@ def extras(ch, s, M):
     gs.close()
     log(f"option pruning: {pruning}")
 
-    return tradeoff, pruning
+    # the smaller workloads: fill time (captured launch sequence replayed, median of 5 after
+    # one warm-up), launches and relaxations per second; launch latency bounds the small ones
+    from paper_2307_01236_amd.chaingen import CONFIGS, make_config_chain
+    others = []
+    for cfg in range(len(CONFIGS)):
+        c = make_config_chain(cfg)
+        if c.name == ch.name:
+            continue
+        cs = rk.Solver(c)
+        fills = []
+        for _ in range(6):
+            cs.solve(c.M)
+            fills.append(cs.fill_ms()[0])
+        ms = statistics.median(fills[1:])
+        others.append({"workload": c.name, "launches": cs.fill_ms()[1], "fill_ms": ms,
+                       "relaxations_per_s": relaxations(c.L, c.K, c.M) / (ms * 1e-3)})
+        cs.close()
+    log(f"other workloads: {others}")
+
+    return tradeoff, pruning, others
 
 
 def main():
@@ -157,7 +178,7 @@ def main():
     ap.add_argument("--config", type=int, default=WORKLOAD_CFG)
     ap.add_argument("--cpu-blocks", type=int, default=144, help="oracle sample size (0: skip)")
     ap.add_argument("--extras", type=int, default=1,
-                    help="0: skip the trade-off and option-pruning reports (other chains' fills)")
+                    help="0: skip the trade-off, option-pruning and other-workload reports")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized buffer 3 times (to scale HBM byte counters) and exit")
     args = ap.parse_args()
@@ -251,9 +272,9 @@ def main():
     s.schedule()
     sched_ms = (time.perf_counter() - t) * 1e3
 
-    tradeoff = pruning = None
+    tradeoff = pruning = others = None
     if args.extras:  # other chains' fills: after the timed and profiled steps
-        tradeoff, pruning = extras(ch, s, M)
+        tradeoff, pruning, others = extras(ch, s, M)
 
     # dominant kernel: the one with the most device time; both of its roofs per launch
     dname, (dn, dms, dwork, dbytes) = max(kern.items(), key=lambda kv: kv[1][1])
@@ -318,7 +339,7 @@ def main():
         "schedule_ms": sched_ms,
         "fill_relax_per_s": relax / (statistics.median(fill_ms) * 1e-3),
         "roofline": roofline, "measured_ceilings": measured, "cpu_baseline": cpu, "tradeoff": tradeoff,
-        "option_pruning": pruning,
+        "option_pruning": pruning, "other_workloads": others,
         "kernels": {k: {"launches_per_step": v[0] / args.steps, "ms_per_step": v[1] / args.steps,
                         "relaxations_per_step": v[2] // args.steps, "table_bytes_per_step": v[3] // args.steps}
                     for k, v in kern.items()},
