@@ -474,7 +474,10 @@ def test_mid_width_four_on_and_off(M):
     try:
         s.set_profiling(True)
         s.solve(M)
-        n_mid = s.kernel_stats()["k_mid"][0]
+        stats = s.kernel_stats()
+        n_mid = stats["k_mid"][0]
+        # the kernels' relaxation counts still add up to the recurrence's candidate count
+        assert sum(v[2] for v in stats.values()) == relaxations(ch.L, ch.K, M)
     finally:
         s.close()
     # mids of width 16 at d = 16, 48 and of width 8 at d = 8, 24, 40, 56; of width 4 at
