@@ -485,6 +485,22 @@ def test_mid_width_four_on_and_off(M):
     assert n_mid == (14 if ch.L * (M + 1) >= 1_600_000 else 6), n_mid
 
 
+@pytest.mark.parametrize("seed", [97003, 97008])
+def test_several_bands_with_width_four_mids(seed):
+    """Chains of 64-110 blocks whose tables pass 1.6e6 blocks x budget columns (78 and 105
+    blocks, one option): two or three band products, mids of widths 16, 8 and 4, and shifts
+    of up to a few hundred columns.  Full-table parity."""
+    rng = np.random.default_rng(seed)
+    L = int(rng.integers(64, 110))
+    K = int(rng.integers(1, 4))
+    M = int(rng.integers(1_600_000 // L, 1_600_000 // L + 3000))
+    ch = make_random_chain(seed, L, K, M=M, xmax=int(rng.integers(1, 300)), amax=int(rng.integers(1, 1500)),
+                           tmax=int(rng.integers(0, 300)), tmin=0, allow_zero=bool(rng.integers(0, 2)),
+                           small_times=bool(rng.integers(0, 2)))
+    assert ch.L * (M + 1) >= 1_600_000
+    full_parity(ch, M)
+
+
 def test_wide_budget():
     """200 001 budget columns on a short chain with large sizes: a left pad of ~2000 columns,
     1 563 column chunks per cell in the finalize and shifts far beyond its staged halo.
