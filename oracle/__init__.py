@@ -22,7 +22,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB = os.path.join(HERE, "librko.so")
 INF = 2**31 - 1
 
-FWD_NOSAVE, FWD_SAVE, BWD, FREE_X = 0, 1, 2, 3
+FWD_NOSAVE, FWD_SAVE, BWD, FREE_X, REFWD = 0, 1, 2, 3, 4
 OK, E_INVAL, E_INFEASIBLE, E_BUFSZ, E_REPLAY = 0, -1, -6, -7, -8
 
 
@@ -39,7 +39,7 @@ def build(force: bool = True) -> str:
 class _Chain(C.Structure):
     _fields_ = [("L", C.c_int32), ("K", C.c_int32)] + [
         (n, C.POINTER(C.c_int32))
-        for n in ("x", "fn_time", "fn_tmp", "fwd", "bwd", "mem", "tmp_fwd", "tmp_bwd")]
+        for n in ("x", "fn_time", "fn_tmp", "fwd", "bwd", "mem", "tmp_fwd", "tmp_bwd", "refwd")]
 
 
 class _Op(C.Structure):
@@ -56,8 +56,9 @@ class Library:
         lib.rko_ncells.restype = C.c_int64
         lib.rko_cell.argtypes = [C.c_int32, C.c_int32, C.c_int32]
         lib.rko_cell.restype = C.c_int64
-        lib.rko_solve.argtypes = [P(_Chain), C.c_int32, P(C.c_int32), P(C.c_int16), P(C.c_int32)]
-        lib.rko_schedule.argtypes = [P(_Chain), C.c_int32, P(C.c_int16), P(_Op), C.c_int64,
+        lib.rko_solve.argtypes = [P(_Chain), C.c_int32, P(C.c_int32), P(C.c_int16), P(C.c_int32),
+                                  P(C.c_int16), P(C.c_int32)]
+        lib.rko_schedule.argtypes = [P(_Chain), C.c_int32, P(C.c_int16), P(C.c_int16), P(_Op), C.c_int64,
                                      P(C.c_int64), P(C.c_int64)]
         lib.rko_simulate.argtypes = [P(_Chain), P(_Op), C.c_int64, P(C.c_int64), P(C.c_int64),
                                      P(C.c_int64)]
@@ -94,11 +95,15 @@ def _i32p(a: np.ndarray):
 
 
 class _Bound:
-    """Keeps the int32 copies alive while the C struct points at them."""
+    """Keeps the int32 copies alive while the C struct points at them.  A chain with a
+    `refwd` array (not None) switches on the saving sweep (rko.h)."""
 
     def __init__(self, ch):
         self.arrs = [np.ascontiguousarray(a, dtype=np.int32).ravel() for a in ch.arrays()]
-        self.s = _Chain(ch.L, ch.K, *[_i32p(a) for a in self.arrs])
+        rf = getattr(ch, "refwd", None)
+        self.refwd = None if rf is None else np.ascontiguousarray(rf, dtype=np.int32).ravel()
+        self.s = _Chain(ch.L, ch.K, *[_i32p(a) for a in self.arrs],
+                        _i32p(self.refwd) if self.refwd is not None else None)
 
 
 def ncells(L: int) -> int:
@@ -121,8 +126,9 @@ def cell_index(L: int) -> np.ndarray:
 
 
 class Solution:
-    def __init__(self, ch, M, opt, arg, answer):
+    def __init__(self, ch, M, opt, arg, answer, hval=None, harg=None):
         self.chain, self.M, self.opt, self.arg, self.answer = ch, M, opt, arg, answer
+        self.hval, self.harg = hval, harg  # the saving sweep's H table and choices, or None
         self.cells = cell_index(ch.L)
 
     def opt_row(self, s: int, t: int) -> np.ndarray:
@@ -135,6 +141,10 @@ class Solution:
         """(opt, arg) as [ncells, M+1] arrays, cells in upper-triangle row-major order."""
         return np.ascontiguousarray(self.opt.T), np.ascontiguousarray(self.arg.T)
 
+    def h_rows(self):
+        """(hval, harg) of the saving sweep as [ncells, M+1] arrays (same order)."""
+        return np.ascontiguousarray(self.hval.T), np.ascontiguousarray(self.harg.T)
+
 
 def solve(ch, M: int | None = None, lib: Library | None = None) -> Solution:
     lib = _load(lib)
@@ -144,11 +154,17 @@ def solve(ch, M: int | None = None, lib: Library | None = None) -> Solution:
     arg = np.empty((M + 1, n), dtype=np.int16)
     ans = C.c_int32(0)
     b = _Bound(ch)
-    rc = lib.rko_solve(C.byref(b.s), M, _i32p(opt), arg.ctypes.data_as(C.POINTER(C.c_int16)),
-                       C.byref(ans))
+    hval = harg = None
+    if b.refwd is not None:
+        hval = np.empty((M + 1, n), dtype=np.int32)
+        harg = np.empty((M + 1, n), dtype=np.int16)
+    i16 = C.POINTER(C.c_int16)
+    rc = lib.rko_solve(C.byref(b.s), M, _i32p(opt), arg.ctypes.data_as(i16),
+                       None if hval is None else _i32p(hval),
+                       None if harg is None else harg.ctypes.data_as(i16), C.byref(ans))
     if rc != OK:
         raise ValueError(f"rko_solve failed: {rc}")
-    return Solution(ch, M, opt, arg, int(ans.value))
+    return Solution(ch, M, opt, arg, int(ans.value), hval, harg)
 
 
 def tradeoff_curve(sol: Solution, n: int | None = None) -> np.ndarray:
@@ -175,14 +191,15 @@ def schedule(sol: Solution, M: int | None = None, lib: Library | None = None):
     b = _Bound(ch)
     # the choice table is laid out for the solve's width; it holds all m <= sol.M
     argp = sol.arg.ctypes.data_as(C.POINTER(C.c_int16))
+    hargp = None if sol.harg is None else sol.harg.ctypes.data_as(C.POINTER(C.c_int16))
     nops, nfwd = C.c_int64(0), C.c_int64(0)
-    rc = lib.rko_schedule(C.byref(b.s), M, argp, None, 0, C.byref(nops), C.byref(nfwd))
+    rc = lib.rko_schedule(C.byref(b.s), M, argp, hargp, None, 0, C.byref(nops), C.byref(nfwd))
     if rc == E_INFEASIBLE:
         return None
     if rc != E_BUFSZ:
         raise ValueError(f"rko_schedule sizing failed: {rc}")
     ops = (_Op * max(1, nops.value))()
-    rc = lib.rko_schedule(C.byref(b.s), M, argp, ops, nops.value, C.byref(nops), C.byref(nfwd))
+    rc = lib.rko_schedule(C.byref(b.s), M, argp, hargp, ops, nops.value, C.byref(nops), C.byref(nfwd))
     if rc != OK:
         raise ValueError(f"rko_schedule failed: {rc}")
     out = np.array([(o.kind, o.block, o.option) for o in ops[:nops.value]], dtype=np.int32)

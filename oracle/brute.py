@@ -4,8 +4,9 @@ Two searches that do not use the dynamic program at all:
 
 * ``decision_trees`` enumerates every schedule of the shape rk-Rotor can
   produce (App. C: at each span either case 1 with some option o, or case 2
-  with some split i, recursively), turns each into its operation list the way
-  Alg. 3 lays it out, and replays it in the oracle's simulator.  The cheapest
+  with some split i, recursively; with a chain's ``refwd`` also the saving
+  sweep with option o and split i, see rko.h), turns each into its operation
+  list the way Alg. 3 lays it out, and replays it in the oracle's simulator.  The cheapest
   replay whose peak fits a budget must equal the dynamic program's value at
   that budget, for every budget: this pins the recurrence, its validity
   conditions and its memory accounting at once.
@@ -22,10 +23,10 @@ import itertools
 
 import numpy as np
 
-from . import BWD, FREE_X, FWD_NOSAVE, FWD_SAVE, INF, simulate
+from . import BWD, FREE_X, FWD_NOSAVE, FWD_SAVE, INF, REFWD, simulate
 
 
-def _trees(L, K, s, t, memo):
+def _trees(L, K, s, t, memo, sweep=False):
     key = (s, t)
     if key in memo:
         return memo[key]
@@ -34,11 +35,18 @@ def _trees(L, K, s, t, memo):
         if s == t:
             out.append(("o", s, o, None))
         else:
-            for sub in _trees(L, K, s + 1, t, memo):
+            for sub in _trees(L, K, s + 1, t, memo, sweep):
                 out.append(("o", s, o, sub))
     for i in range(s + 1, t + 1):
-        for right, left in itertools.product(_trees(L, K, i, t, memo), _trees(L, K, s, i - 1, memo)):
+        for right, left in itertools.product(_trees(L, K, i, t, memo, sweep),
+                                             _trees(L, K, s, i - 1, memo, sweep)):
             out.append(("i", s, i, (right, left)))
+    if sweep:  # F_s^o, sweep s+1..i-1 to x_i, i..t, x_{s+1} again from F_s^o's data, s+1..i-1, B_s^o
+        for o in range(K):
+            for i in range(s + 2, t + 1):
+                for right, left in itertools.product(_trees(L, K, i, t, memo, sweep),
+                                                     _trees(L, K, s + 1, i - 1, memo, sweep)):
+                    out.append(("h", s, (o, i), (right, left)))
     memo[key] = out
     return out
 
@@ -50,6 +58,18 @@ def _ops(tree, acc):
         if sub is not None:
             _ops(sub, acc)
         acc.append((BWD, s, v))
+    elif kind == "h":
+        o, i = v
+        right, left = sub
+        acc.append((FWD_SAVE, s, o))
+        for k in range(s + 1, i):
+            acc.append((FWD_NOSAVE, k, -1))
+            acc.append((FREE_X, k, -1))
+        _ops(right, acc)
+        acc.append((FREE_X, i, -1))
+        acc.append((REFWD, s, o))
+        _ops(left, acc)
+        acc.append((BWD, s, o))
     else:
         i = v
         right, left = sub
@@ -63,14 +83,16 @@ def _ops(tree, acc):
     return acc
 
 
-def count_trees(L: int, K: int) -> int:
-    return len(_trees(L, K, 0, L - 1, {}))
+def count_trees(L: int, K: int, sweep: bool = False) -> int:
+    return len(_trees(L, K, 0, L - 1, {}, sweep))
 
 
 def decision_trees(ch, Mmax: int, lib=None) -> np.ndarray:
-    """best[M] for M = 0..Mmax: cheapest rk-Rotor-shaped schedule with peak <= M (INF if none)."""
+    """best[M] for M = 0..Mmax: cheapest rk-Rotor-shaped schedule with peak <= M (INF if none).
+    A chain with a ``refwd`` array also gets the saving sweep's trees."""
     best = np.full(Mmax + 1, INF, dtype=np.int64)
-    for tree in _trees(ch.L, ch.K, 0, ch.L - 1, {}):
+    sweep = getattr(ch, "refwd", None) is not None
+    for tree in _trees(ch.L, ch.K, 0, ch.L - 1, {}, sweep):
         ops = _ops(tree, [])
         ok, tm, pk, _ = simulate(ch, ops, lib=lib)
         assert ok, "an rk-Rotor-shaped schedule must always replay legally"
@@ -80,8 +102,10 @@ def decision_trees(ch, Mmax: int, lib=None) -> np.ndarray:
 
 
 def dijkstra_lower_bound(ch, M: int) -> int:
-    """Cheapest legal operation order with every operation's peak <= M (INF if none)."""
+    """Cheapest legal operation order with every operation's peak <= M (INF if none).  With
+    a chain's ``refwd``, making x_{k+1} again from F_k^o's kept data is one more move."""
     L, K = ch.L, ch.K
+    refwd = getattr(ch, "refwd", None)
     x = [int(v) for v in ch.x]
     mem = ch.mem.astype(np.int64)
     if x[0] > M:
@@ -119,6 +143,10 @@ def dijkstra_lower_bound(ch, M: int) -> int:
             if live(xm, k) and not live(xm, k + 1):
                 if u + x[k + 1] + int(ch.fn_tmp[k]) <= M:
                     nxt.append((int(ch.fn_time[k]), (xm | 1 << (k + 1), h, g)))
+                if refwd is not None and h[k] >= 0:
+                    o = h[k]
+                    if u + x[k + 1] + int(ch.tmp_fwd[k, o]) <= M:
+                        nxt.append((int(refwd[k, o]), (xm | 1 << (k + 1), h, g)))
                 if h[k] < 0:
                     for o in range(K):
                         if u + x[k + 1] + int(mem[k, o]) + int(ch.tmp_fwd[k, o]) <= M:

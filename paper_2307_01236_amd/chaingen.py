@@ -29,7 +29,7 @@ import hashlib
 import numpy as np
 
 __all__ = ["Chain", "CONFIGS", "make_config_chain", "make_random_chain", "make_grid_chain",
-           "config_by_name"]
+           "config_by_name", "with_refwd"]
 
 
 @dataclasses.dataclass
@@ -43,6 +43,9 @@ class Chain:
     mem      [L,K]  size of the intermediates option o keeps for its backward
     tmp_fwd, tmp_bwd [L,K]  tmp(F_i^o), tmp(B_i^o)
     M        budget (memory slots) the workload is solved at
+    refwd    [L,K]  or None: time to compute x_{i+1} again from the intermediates F_i^o
+             kept (the saving sweep of the paper's sub-optimality remark (ii), Sec. 3.4);
+             None leaves it out
     """
 
     L: int
@@ -57,6 +60,7 @@ class Chain:
     tmp_bwd: np.ndarray
     M: int
     name: str = "chain"
+    refwd: np.ndarray | None = None
 
     def arrays(self):
         return (self.x, self.fn_time, self.fn_tmp, self.fwd, self.bwd, self.mem,
@@ -67,6 +71,9 @@ class Chain:
         h.update(np.array([self.L, self.K, self.M], dtype=np.int64).tobytes())
         for a in self.arrays():
             h.update(np.ascontiguousarray(a, dtype=np.int32).tobytes())
+        if self.refwd is not None:
+            h.update(b"refwd")
+            h.update(np.ascontiguousarray(self.refwd, dtype=np.int32).tobytes())
         return h.hexdigest()
 
     def sub(self, s: int, t: int) -> "Chain":
@@ -76,7 +83,8 @@ class Chain:
                      fwd=self.fwd[s:t + 1].copy(), bwd=self.bwd[s:t + 1].copy(),
                      mem=self.mem[s:t + 1].copy(), tmp_fwd=self.tmp_fwd[s:t + 1].copy(),
                      tmp_bwd=self.tmp_bwd[s:t + 1].copy(), M=self.M,
-                     name=f"{self.name}[{s}:{t}]")
+                     name=f"{self.name}[{s}:{t}]",
+                     refwd=None if self.refwd is None else self.refwd[s:t + 1].copy())
 
     def options(self, keep) -> "Chain":
         """The same blocks with only the saving options listed in `keep` (in that order).
@@ -87,7 +95,8 @@ class Chain:
         return Chain(L=self.L, K=len(keep), x=self.x.copy(), fn_time=self.fn_time.copy(),
                      fn_tmp=self.fn_tmp.copy(), fwd=pick(self.fwd), bwd=pick(self.bwd),
                      mem=pick(self.mem), tmp_fwd=pick(self.tmp_fwd), tmp_bwd=pick(self.tmp_bwd),
-                     M=self.M, name=f"{self.name}{{options {keep}}}")
+                     M=self.M, name=f"{self.name}{{options {keep}}}",
+                     refwd=None if self.refwd is None else pick(self.refwd))
 
 # name, L, K, M, block-structure kind
 CONFIGS = [
@@ -199,6 +208,16 @@ def make_random_chain(seed: int, L: int, K: int, *, M: int | None = None, xmax: 
         M = int(x.sum() + mem.max(axis=1).sum() + tf.max() + tb.max() + 2)
     return Chain(L=L, K=K, x=_i32(x), fn_time=fn_time, fn_tmp=fn_tmp, fwd=fwd, bwd=bwd,
                  mem=mem, tmp_fwd=tf, tmp_bwd=tb, M=int(M), name=f"random{seed}_L{L}_K{K}")
+
+
+def with_refwd(ch: Chain, seed: int, lo: float = 0.0, hi: float = 1.0) -> Chain:
+    """The same chain with re-forward times for the saving sweep: recomputing x_{i+1} from
+    the intermediates option o kept costs floor(r(F_i^0) * U[lo, hi]) (input synthesis
+    only; hi <= 1 keeps it below a full forward)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    u = rng.uniform(lo, hi, size=(ch.L, ch.K))
+    refwd = np.floor(ch.fn_time.astype(np.float64)[:, None] * u).astype(np.int64)
+    return dataclasses.replace(ch, refwd=_i32(refwd), name=f"{ch.name}+refwd{seed}")
 
 
 def _grid_options(rng, n_peak: int, n_save: int):

@@ -1,0 +1,237 @@
+"""Pins of the oracle's saving sweep (no GPU).
+
+The saving sweep is this build's reading of the sub-optimality remark (ii) of Sec. 3.4:
+a forward that runs more than once may keep intermediate data on its first pass and make
+its output faster on later passes.  Case 3 of a span (s,t) keeps F_s^o's intermediates
+through a no-save sweep from s+1 (which, unlike case 2's, also drops x_{s+1}), makes
+x_{s+1} again from them in refwd time and finishes with B_s^o (rko.h gives the
+recurrence).  The pins do not reuse that recurrence: a hand-derived example, exhaustive
+enumeration of every schedule shape (cases 1, 2 and 3, recursively) replayed in the
+simulator, Dijkstra over all legal operation orders with the re-forward as a move, the
+feasibility recursion, and relations to the unwidened recurrence.
+"""
+import dataclasses
+import json
+import os
+
+import numpy as np
+
+import oracle
+from oracle import brute
+from paper_2307_01236_amd.chaingen import Chain, make_random_chain, with_refwd
+
+INF = oracle.INF
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+KIND = {"FWD_NOSAVE": oracle.FWD_NOSAVE, "FWD_SAVE": oracle.FWD_SAVE, "BWD": oracle.BWD,
+        "FREE_X": oracle.FREE_X, "REFWD": oracle.REFWD}
+
+
+def _i32(a):
+    return np.asarray(a, dtype=np.int32)
+
+
+def sweep_example():
+    g = json.load(open(os.path.join(GOLDEN, "saving_sweep_example_L3.json")))
+    c = g["chain"]
+    ch = Chain(L=c["L"], K=c["K"], x=_i32(c["x"]), fn_time=_i32(c["fn_time"]), fn_tmp=_i32(c["fn_tmp"]),
+               fwd=_i32(c["fwd"]), bwd=_i32(c["bwd"]), mem=_i32(c["mem"]), tmp_fwd=_i32(c["tmp_fwd"]),
+               tmp_bwd=_i32(c["tmp_bwd"]), M=g["M"], name="sweep_example", refwd=_i32(c["refwd"]))
+    return g, ch
+
+
+def tiny_sweep_chains(n=30, seed0=0):
+    """Chains small enough to enumerate every schedule shape (L <= 5), with re-forward
+    times from zero (the sweep is free) to a full forward, ties included; every third
+    one has backward temporaries well above the forward ones."""
+    out = []
+    for seed in range(seed0, seed0 + n):
+        rng = np.random.default_rng(7000 + seed)
+        L = int(rng.integers(1, 6))
+        K = int(rng.integers(1, 3)) if L == 5 else int(rng.integers(1, 4))
+        ch = make_random_chain(7000 + seed, L, K, M=40, allow_zero=seed % 3 == 0, small_times=seed % 2 == 0,
+                               xmax=6, amax=8, tmax=4, independent_tmp=seed % 4 != 1)
+        if seed % 3 == 2:
+            ch = dataclasses.replace(ch, tmp_bwd=_i32(ch.tmp_bwd + rng.integers(0, 8, size=ch.tmp_bwd.shape)))
+        out.append(with_refwd(ch, seed, 0.0, 1.0 if seed % 5 else 0.0))
+    return out
+
+
+def mid_sweep_chains():
+    return [with_refwd(make_random_chain(400 + s, L, K, allow_zero=s % 2 == 0, xmax=10), s, 0.0, 0.6)
+            for s, (L, K) in enumerate([(8, 3), (13, 1), (20, 4), (25, 2), (6, 8), (1, 5), (3, 2)])]
+
+
+# ---- hand-derived example ------------------------------------------------------------------
+
+def check_sweep_example(lib=None):
+    g, ch = sweep_example()
+    sol = oracle.solve(ch, lib=lib)
+    row, arg = sol.opt_row(0, 2), sol.arg_row(0, 2)
+    for seg in g["opt_0_2"]:
+        sl = slice(seg["m_lo"], seg["m_hi"] + 1)
+        val = INF if seg["value"] == "inf" else seg["value"]
+        assert (row[sl] == val).all() and (arg[sl] == seg["code"]).all(), seg
+    hrow = sol.hval[:, sol.cells[1, 2]]
+    harg = sol.harg[:, sol.cells[1, 2]]
+    for seg in g["h_1_2"]:
+        sl = slice(seg["u_lo"], seg["u_hi"] + 1)
+        val = INF if seg["value"] == "inf" else seg["value"]
+        assert (hrow[sl] == val).all() and (harg[sl] == seg["code"]).all(), seg
+    plain = oracle.solve(Chain(**{**ch.__dict__, "refwd": None}), lib=lib)
+    assert plain.opt_row(0, 2)[8] == g["without_sweep_opt_0_2_at_8"]
+    assert oracle.min_feasible(ch, lib=lib)[sol.cells[0, 2]] == g["min_budget_0_2"]
+    exp = g["schedule_at_M8"]
+    ops, nfwd = oracle.schedule(sol, 8, lib=lib)
+    want = np.array([(KIND[k], b, o) for k, b, o in exp["ops"]], dtype=np.int32)
+    assert np.array_equal(ops, want) and nfwd == exp["n_fwd"], ops
+    ok, tm, pk, _ = oracle.simulate(ch, ops, lib=lib)
+    assert ok and tm == exp["time"] and pk == exp["peak"]
+    tie = g["tie_with_refwd_10"]
+    ch10 = Chain(**{**ch.__dict__, "refwd": np.full((ch.L, ch.K), tie["refwd"], dtype=np.int32)})
+    sol10 = oracle.solve(ch10, lib=lib)
+    assert sol10.opt_row(0, 2)[tie["m"]] == tie["value"] and sol10.arg_row(0, 2)[tie["m"]] == tie["code"]
+    tb = g["tight_backward_temp"]
+    tmpb = ch.tmp_bwd.copy()
+    tmpb[0, 0] = tb["tmp_bwd_block0"]
+    chb = Chain(**{**ch.__dict__, "tmp_bwd": tmpb})
+    solb = oracle.solve(chb, lib=lib)
+    rowb = solb.opt_row(0, 2)
+    assert (rowb[:tb["inf_up_to_m"] + 1] == INF).all()
+    assert rowb[tb["m_min"]] == tb["value_at_9"] and solb.arg_row(0, 2)[tb["m_min"]] == tb["code_at_9"]
+    assert oracle.min_feasible(chb, lib=lib)[solb.cells[0, 2]] == tb["m_min"]
+    check_simulator_refwd_peak(lib)
+
+
+def check_simulator_refwd_peak(lib=None):
+    """The re-forward's peak is its own: with x_2 still live (an order no rk-Rotor shape
+    makes), x_1 and tmp(F_0^0) come on top of it (hand-counted: 0 + 1 + 1 + 5 + 3 = 10,
+    above F_0^0's 9)."""
+    g, ch = sweep_example()
+    tmpf = ch.tmp_fwd.copy()
+    tmpf[0, 0] = 3
+    chf = Chain(**{**ch.__dict__, "tmp_fwd": tmpf})
+    ops = np.array([(oracle.FWD_SAVE, 0, 0), (oracle.FWD_NOSAVE, 1, -1), (oracle.FREE_X, 1, -1),
+                    (oracle.REFWD, 0, 0)], dtype=np.int32)
+    ok, tm, pk, bad = oracle.simulate(chf, ops, lib=lib)
+    assert not ok and bad == len(ops)  # legal steps, unfinished schedule
+    assert pk == 10 and tm == 10 + 10 + 2
+
+
+def test_sweep_example():
+    check_sweep_example()
+
+
+# ---- exhaustive enumeration ----------------------------------------------------------------
+
+def test_tree_count_with_sweep():
+    """T(0) = 1 (empty rest), T(n) = K T(n-1) + sum_{j=1}^{n-1} T(n-j) T(j)
+    + K sum_{j=2}^{n-1} T(n-j) T(j-1), counted independently of the enumerator."""
+    for K in (1, 2, 3):
+        T = [1]
+        for n in range(1, 6):
+            T.append(K * T[n - 1] + sum(T[n - j] * T[j] for j in range(1, n))
+                     + K * sum(T[n - j] * T[j - 1] for j in range(2, n)))
+        for n in range(1, 6):
+            assert brute.count_trees(n, K, sweep=True) == T[n], (n, K)
+    assert brute.count_trees(3, 2, sweep=True) == 56  # 48 without the sweep, 8 sweep trees
+
+
+def check_bruteforce_sweep(chains, lib=None):
+    import test_oracle as T
+    T.check_bruteforce(chains, lib)
+
+
+def test_bruteforce_all_spans_with_sweep():
+    check_bruteforce_sweep(tiny_sweep_chains(30))
+
+
+def test_sweep_is_used():
+    """The widening matters: on these chains some optimum strictly drops and some recorded
+    choice is a saving sweep (code >= L + K)."""
+    lower = used = 0
+    for ch in tiny_sweep_chains(30) + mid_sweep_chains():
+        sol = oracle.solve(ch)
+        base = oracle.solve(Chain(**{**ch.__dict__, "refwd": None}))
+        a, b = sol.opt.astype(np.int64), base.opt.astype(np.int64)
+        assert (a <= b).all(), ch.name  # a wider choice set never costs more
+        lower += int((a < b).sum())
+        used += int((sol.arg >= ch.L + ch.K).sum())
+    assert lower > 0 and used > 0
+
+
+def test_costly_refwd_changes_only_infeasible_cells():
+    """With a re-forward dearer than any schedule, the sweep can only fill cells the
+    unwidened recurrence leaves infinite (tight budgets where x_{s+1} cannot stay live)."""
+    for ch in mid_sweep_chains():
+        big = Chain(**{**ch.__dict__, "refwd": np.full((ch.L, ch.K), 1 << 26, dtype=np.int32)})
+        a = oracle.solve(big).opt.astype(np.int64)
+        b = oracle.solve(Chain(**{**ch.__dict__, "refwd": None})).opt.astype(np.int64)
+        fin = b < INF
+        assert np.array_equal(a[fin], b[fin]), ch.name
+        assert (a[~fin & (a < INF)] >= 1 << 26).all()
+
+
+def test_dijkstra_lower_bound_with_refwd():
+    total = 0
+    for ch in tiny_sweep_chains(20, seed0=100):
+        if ch.L > 4:
+            continue
+        for M in range(0, 41, 8):
+            lb = brute.dijkstra_lower_bound(ch, M)
+            a = oracle.solve(ch, M).answer
+            assert lb <= a
+            assert (lb == INF) == (a == INF) or a == INF
+            total += 1
+    assert total > 30
+
+
+# ---- feasibility, monotonicity, replays ------------------------------------------------------
+
+def check_inf_pattern_sweep(chains, lib=None):
+    import test_oracle as T
+    T.check_inf_pattern(chains, lib)
+
+
+def test_inf_pattern_with_sweep():
+    check_inf_pattern_sweep(mid_sweep_chains() + tiny_sweep_chains(10))
+
+
+def test_monotone_in_budget_with_sweep():
+    for ch in mid_sweep_chains():
+        opt = oracle.solve(ch).opt.astype(np.int64)
+        assert (opt[1:] <= opt[:-1]).all(), ch.name
+
+
+def check_replay_sweep(chains, lib=None):
+    """Alg. 3's schedule at every budget replays legally, in the optimum's time and within
+    the budget."""
+    seen = 0
+    for ch in chains:
+        sol = oracle.solve(ch, lib=lib)
+        for M in range(sol.M + 1):
+            ans = int(sol.opt_row(0, ch.L - 1)[M - ch.x[0]]) if M >= ch.x[0] else INF
+            sched = oracle.schedule(sol, M, lib=lib)
+            if ans == INF:
+                assert sched is None
+                continue
+            ops, _ = sched
+            ok, tm, pk, bad = oracle.simulate(ch, ops, lib=lib)
+            assert ok, (ch.name, M, bad)
+            assert tm == ans and pk <= M, (ch.name, M, tm, ans, pk)
+            seen += int((ops[:, 0] == oracle.REFWD).any())
+    return seen
+
+
+def test_schedule_replay_with_sweep():
+    assert check_replay_sweep(mid_sweep_chains()) > 0
+
+
+def test_simulator_rejects_refwd_without_kept_data():
+    g, ch = sweep_example()
+    bad = np.array([(oracle.REFWD, 0, 0)], dtype=np.int32)
+    ok, _, _, idx = oracle.simulate(ch, bad)
+    assert not ok and idx == 0
+    plain = Chain(**{**ch.__dict__, "refwd": None})
+    ops = np.array([(KIND[k], b, o) for k, b, o in g["schedule_at_M8"]["ops"]], dtype=np.int32)
+    ok, _, _, idx = oracle.simulate(plain, ops)  # no re-forward times: the op is illegal
+    assert not ok and ops[idx, 0] == oracle.REFWD
