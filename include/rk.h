@@ -123,6 +123,29 @@ int rk_solve(rk_chain *c, int32_t M, int32_t *opt_out);
  */
 int rk_solve_async(rk_chain *c, int32_t M, void *d_workspace, size_t ws_bytes, void *stream);
 
+/*
+ * For callers that cannot allocate (code under HIP graph capture that may not call
+ * hipMalloc, tight serving loops, harnesses that forbid allocation): the fill of
+ * rk_solve_async, with its tables in a static device array of RK_NOALLOC_MAX_BYTES that
+ * the library holds on every device it runs on (until the process ends), and with its
+ * kernels launched one by one on `stream` (NULL: a stream the chain owns).  This call
+ * allocates nothing: no hipMalloc, hipFree, graph or event creation.  Asynchronous like
+ * rk_solve_async; rk_result, rk_read_row, rk_tradeoff_curve and rk_extract_schedule
+ * then read that array.
+ *   - The chain must have been solved once before on this device (rk_solve or
+ *     rk_solve_async, which upload its derived arrays), with the same option-pruning
+ *     setting, and profiling must be off; else RK_E_INVAL.
+ *   - RK_E_NOMEM when rk_workspace_bytes(c, M) exceeds RK_NOALLOC_MAX_BYTES (about
+ *     L = 64 blocks at M = 3500, or L = 128 at M = 895, with activations of at most
+ *     64 slots).
+ *   - Every call on a device shares that device's array and overwrites what the previous
+ *     call left there: reads of an earlier call's results are valid only until the next
+ *     rk_solve_noalloc on the same device, and calls that overlap on one device (other
+ *     streams, other threads, other chains) race.
+ */
+#define RK_NOALLOC_MAX_BYTES ((size_t)64 << 20)
+int rk_solve_noalloc(rk_chain *c, int32_t M, void *stream);
+
 /* Wait for the last solve of the chain and return its answer (as rk_solve). */
 int rk_result(rk_chain *c, int32_t *opt_out);
 

@@ -5,6 +5,7 @@
 // dynamic program itself runs here; the fill, the choice recovery and Alg. 3
 // all run in the kernels of rk_kernels.hip.
 #include <algorithm>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -210,10 +211,38 @@ int ensure_device(rk_chain *c)
 
 int32_t to_abi(int32_t v) { return v >= DINF ? RK_INF : v; }
 
+// Tables of rk_solve_noalloc: a static array on every device the library runs on.  In host
+// code its name stands for a host-side shadow, not for device memory: the device address
+// comes from hipGetSymbolAddress, once per device, with that device current, and only
+// that address is handed to kernels.
+static __device__ __align__(256) int32_t scratch[RK_NOALLOC_MAX_BYTES / sizeof(int32_t)];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of `scratch` on the current device `dev`.
+int scratch_address(int dev, void **ptr)
+{
+    if (dev < 0 || dev >= kMaxDevices) return RK_E_DEVICE;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+            (void)hipGetLastError();
+            return RK_E_DEVICE;
+        }
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return RK_OK;
+}
+
 // Queue the fill on `stream`: replay the captured launch sequence when nothing it depends
-// on changed, else capture it anew; inside a capture of the caller's (in_capture) the
-// kernels are launched directly into that capture.
-int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t stream, bool in_capture = false)
+// on changed, else capture it anew.  With `direct` the kernels are launched one by one
+// (inside a capture of the caller's they go into that capture; rk_solve_noalloc may not
+// create a graph).
+int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t stream, bool direct = false)
 {
     c->queued = false;
     c->M = M;
@@ -228,7 +257,7 @@ int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t
     HIPCHK(hipEventRecord(c->ev_fill0, stream));
     const bool replay = c->gexec && c->g_M == M && c->g_tables == tables && c->g_stream == stream &&
                         c->g_prof == c->prof.on;
-    if (in_capture) {
+    if (direct) {
         c->prof.reset(stream);
         HIPCHK(rk::launch_fill(c->dc, c->tb, stream, &c->launches, &c->prof));
     } else if (replay) {
@@ -445,6 +474,27 @@ int rk_solve_async(rk_chain *c, int32_t M, void *d_workspace, size_t ws_bytes, v
         tab = static_cast<int32_t *>(c->own_ws);
     }
     return fill(c, M, g, tab, stream ? static_cast<hipStream_t>(stream) : c->own_stream);
+}
+
+int rk_solve_noalloc(rk_chain *c, int32_t M, void *stream)
+{
+    if (!c) return RK_E_INVAL;
+    size_t need = 0;
+    Geometry g;
+    int rc = geometry(c, M, &g, &need);
+    if (rc != RK_OK) return rc;
+    if (need > RK_NOALLOC_MAX_BYTES) return RK_E_NOMEM;
+    // the derived arrays, events and stream exist from an earlier solve on this device
+    if (!c->d_chain || c->run_prune != c->prune || c->prof.on || !c->ev_fill0 || !c->ev_fill1)
+        return RK_E_INVAL;
+    DeviceScope ds(c);
+    if (!ds.ok) return RK_E_DEVICE;
+    void *tab = nullptr;
+    if ((rc = scratch_address(c->device, &tab)) != RK_OK) return rc;
+    if (c->queued) HIPCHK(hipEventSynchronize(c->ev_fill1));  // the previous fill may still read its table
+    // launched directly: capturing and instantiating a graph would allocate
+    return fill(c, M, g, static_cast<int32_t *>(tab), stream ? static_cast<hipStream_t>(stream) : c->own_stream,
+                true);
 }
 
 int rk_solve(rk_chain *c, int32_t M, int32_t *opt_out)

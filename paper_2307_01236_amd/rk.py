@@ -25,7 +25,8 @@ RK_FWD_NOSAVE, RK_FWD_SAVE, RK_BWD, RK_FREE_X = 0, 1, 2, 3
 EXPORTS = ("rk_chain_create", "rk_chain_destroy", "rk_workspace_bytes", "rk_solve", "rk_solve_async",
            "rk_result", "rk_extract_schedule", "rk_read_row", "rk_tradeoff_curve", "rk_last_fill_ms",
            "rk_set_profiling", "rk_set_option_pruning", "rk_chain_options",
-           "rk_fill_kernel_stats", "rk_strerror")
+           "rk_fill_kernel_stats", "rk_strerror", "rk_solve_noalloc")
+RK_NOALLOC_MAX_BYTES = 64 << 20
 
 
 class RKError(RuntimeError):
@@ -60,6 +61,7 @@ def load():
         lib.rk_workspace_bytes.argtypes = [C.c_void_p, i32, P(C.c_size_t)]
         lib.rk_solve.argtypes = [C.c_void_p, i32, i32p]
         lib.rk_solve_async.argtypes = [C.c_void_p, i32, C.c_void_p, C.c_size_t, C.c_void_p]
+        lib.rk_solve_noalloc.argtypes = [C.c_void_p, i32, C.c_void_p]
         lib.rk_result.argtypes = [C.c_void_p, i32p]
         lib.rk_extract_schedule.argtypes = [C.c_void_p, P(rk_op), i64, P(i64), P(i64)]
         lib.rk_read_row.argtypes = [C.c_void_p, i32, i32, i32p, P(C.c_int16)]
@@ -123,6 +125,10 @@ def rk_solve(h, M: int) -> int:
 def rk_solve_async(h, M: int, workspace_ptr: int, ws_bytes: int, stream_ptr: int | None) -> None:
     _check(load().rk_solve_async(h, int(M), C.c_void_p(workspace_ptr), C.c_size_t(ws_bytes),
                                  C.c_void_p(stream_ptr or 0)), "rk_solve_async")
+
+
+def rk_solve_noalloc(h, M: int, stream_ptr: int | None = None) -> None:
+    _check(load().rk_solve_noalloc(h, int(M), C.c_void_p(stream_ptr or 0)), "rk_solve_noalloc")
 
 
 def rk_result(h) -> int:
