@@ -176,39 +176,94 @@ def sub_rows_parity(s, ch, s0, n):
             assert np.array_equal(g_arg.astype(np.int32), exp), (s0 + a, s0 + b)
 
 
-@pytest.mark.parametrize("cfg", [3, 4])
-def test_large_configs_sampled_and_properties(cfg):
-    """Full-size solve; exact parity on sampled sub-chains; properties on the whole table."""
-    ch = make_config_chain(cfg)
-    say(f"  solving {ch.name}")
+def check_properties(ch, opt, M):
+    """Whole-table properties that hold at any size: the infeasibility pattern of the
+    budget-free recursion, Opt non-increasing in m, and the store-all lower bound."""
+    mf = oracle.min_feasible(ch)
+    m = np.arange(M + 1)
+    assert np.array_equal(opt != INF, m[None, :] >= mf[:, None])
+    assert (opt[:, 1:] <= opt[:, :-1]).all()  # INF is INT32_MAX: the int32 order is the order
+    top = opt[oracle.cell_index(ch.L)[0, ch.L - 1]]
+    lb = (ch.fwd.astype(np.int64) + ch.bwd).min(axis=1).sum()
+    assert (top[top != INF] >= lb).all()
+
+
+def test_config3_full_table_against_oracle():
+    """Configuration 3 (L=256, K=8, M=4000: 1.2e10 candidates) at full size: every Opt and
+    choice row, the answer and the schedule against the oracle run in this process."""
+    ch = make_config_chain(3)
+    say(f"  solving {ch.name} on the GPU")
     s = rk.Solver(ch)
     try:
         ans = s.solve()
-        assert ans != INF
-        for s0, n in ((0, 24), (ch.L // 2, 20), (ch.L - 24, 24)):
-            sub_rows_parity(s, ch, s0, n)
-        # schedule: replays legally in the oracle's simulator at exactly the optimum
+        g_opt, g_arg = s.rows()
         ops, nfwd = s.schedule()
-        ok, tm, pk, bad = oracle.simulate(ch, ops)
-        assert ok, bad
-        assert tm == ans and pk <= ch.M
-        # infeasibility pattern and monotonicity on sampled rows
-        mf = oracle.min_feasible(ch)
-        cells = oracle.cell_index(ch.L)
-        rng = np.random.default_rng(cfg)
-        m = np.arange(ch.M + 1)
-        for _ in range(60):
-            a = int(rng.integers(0, ch.L))
-            b = int(rng.integers(a, ch.L))
-            row, _ = s.row(a, b, want_arg=False)
-            assert np.array_equal(row != INF, m >= mf[cells[a, b]]), (a, b)
-            r64 = row.astype(np.int64)
-            assert (r64[1:] <= r64[:-1]).all(), (a, b)
-        row, _ = s.row(0, ch.L - 1, want_arg=False)
-        lb = (ch.fwd.astype(np.int64) + ch.bwd).min(axis=1).sum()
-        assert (row[row != INF] >= lb).all()
     finally:
         s.close()
+    say("  oracle ...")
+    sol = oracle.solve(ch)
+    assert ans == sol.answer, (ans, sol.answer)
+    o_opt, o_arg = sol.rows()
+    cells = oracle.cell_index(ch.L)
+    for name, g, o in (("Opt", g_opt, o_opt), ("choice", g_arg, o_arg)):
+        bad = np.argwhere(g != o)
+        if bad.size:
+            k, m = bad[0]
+            s_, t_ = map(int, np.argwhere(cells == k)[0])
+            raise AssertionError(f"{name} differs at {len(bad)} entries, first (s,t,m)=({s_},{t_},{m}): "
+                                 f"GPU {g[k, m]} oracle {o[k, m]}")
+    exp_ops, exp_nfwd = oracle.schedule(sol)
+    assert np.array_equal(ops, exp_ops) and nfwd == exp_nfwd
+    ok, tm, pk, _ = oracle.simulate(ch, ops)
+    assert ok and tm == ans and pk <= ch.M
+    check_properties(ch, g_opt, ch.M)
+
+
+def test_config4_full_table_against_oracle_digests():
+    """Configuration 4 (L=384, K=16, M=6000: 4.4e8 cells) at full size, in the launch
+    configuration the benchmark times: every Opt and choice row against per-row digests of
+    the oracle's tables (tests/golden/config4_*, written by make_config_digests.py from the
+    oracle alone), the answer and the schedule against the oracle's.  A differing row is
+    recomputed by the oracle on its own blocks, which names the first differing (s, t, m)."""
+    import json
+    import os
+    from rowdigest import arg_digests, opt_digests
+    gold = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+    with open(os.path.join(gold, "config4_oracle.json")) as f:
+        meta = json.load(f)
+    dig = np.load(os.path.join(gold, "config4_row_digests.npz"))
+    ch = make_config_chain(4)
+    assert ch.sha256() == meta["chain_sha256"], "the generator no longer draws the stored chain"
+    say(f"  solving {ch.name} on the GPU")
+    s = rk.Solver(ch)
+    try:
+        ans = s.solve()
+        g_opt, g_arg = s.rows()
+        ops, nfwd = s.schedule()
+    finally:
+        s.close()
+    assert ans == meta["answer"], (ans, meta["answer"])
+    god, gad = opt_digests(g_opt), arg_digests(g_arg)
+    bad = np.flatnonzero((god != dig["opt"]) | (gad != dig["arg"]))
+    if bad.size:
+        cells = oracle.cell_index(ch.L)
+        spans = [tuple(map(int, np.argwhere(cells == k)[0])) for k in bad]
+        s_, t_ = min(spans, key=lambda st: (st[1] - st[0], st[0]))  # the shortest differing span
+        k = int(cells[s_, t_])
+        sub = oracle.solve(ch.sub(s_, t_))
+        o_opt = sub.opt_row(0, t_ - s_)
+        o_arg = sub.arg_row(0, t_ - s_).astype(np.int32)
+        n = t_ - s_ + 1
+        o_arg = np.where(o_arg < 0, -1, np.where(o_arg >= n, o_arg - n + ch.L, o_arg + s_))
+        where = np.flatnonzero((g_opt[k] != o_opt) | (g_arg[k].astype(np.int32) != o_arg))
+        m = int(where[0]) if where.size else -1
+        raise AssertionError(f"{bad.size} rows differ from the oracle's digests; shortest differing span "
+                             f"({s_},{t_}), first differing m={m}: GPU Opt/choice "
+                             f"{g_opt[k, m]}/{g_arg[k, m]}, oracle {o_opt[m]}/{o_arg[m]}")
+    assert np.array_equal(ops, np.asarray(meta["schedule"], dtype=np.int32)) and nfwd == meta["n_fwd"]
+    ok, tm, pk, _ = oracle.simulate(ch, ops)
+    assert ok and tm == ans and pk <= ch.M
+    check_properties(ch, g_opt, ch.M)
 
 
 def test_profiling_counts_launches():
