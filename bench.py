@@ -254,12 +254,13 @@ def main():
     kern = {}
     for i in range(args.steps):
         step()
-        for name, (n, ms, work, moved) in s.kernel_stats().items():
-            a = kern.setdefault(name, [0, 0.0, 0, 0])
+        for name, (n, ms, work, evaluated, moved) in s.kernel_stats().items():
+            a = kern.setdefault(name, [0, 0.0, 0, 0, 0])
             a[0] += n
             a[1] += ms
             a[2] += work
-            a[3] += moved
+            a[3] += evaluated
+            a[4] += moved
     s.set_profiling(False)
 
     # solve wall time without the schedule, warm (synchronous rk_solve on the library's table)
@@ -277,7 +278,7 @@ def main():
         tradeoff, pruning, others = extras(ch, s, M)
 
     # dominant kernel: the one with the most device time; both of its roofs per launch
-    dname, (dn, dms, dwork, dbytes) = max(kern.items(), key=lambda kv: kv[1][1])
+    dname, (dn, dms, _, dwork, dbytes) = max(kern.items(), key=lambda kv: kv[1][1])
     per_launch_s = dms / dn * 1e-3
     ops_per_launch = OPS_PER_RELAX * dwork / dn
     bytes_per_launch = dbytes / dn
@@ -341,7 +342,8 @@ def main():
         "roofline": roofline, "measured_ceilings": measured, "cpu_baseline": cpu, "tradeoff": tradeoff,
         "option_pruning": pruning, "other_workloads": others,
         "kernels": {k: {"launches_per_step": v[0] / args.steps, "ms_per_step": v[1] / args.steps,
-                        "relaxations_per_step": v[2] // args.steps, "table_bytes_per_step": v[3] // args.steps}
+                        "relaxations_per_step": v[2] // args.steps, "evaluated_per_step": v[3] // args.steps,
+                        "table_bytes_per_step": v[4] // args.steps}
                     for k, v in kern.items()},
     }
     s.close()

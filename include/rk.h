@@ -190,21 +190,27 @@ int rk_last_fill_ms(rk_chain *c, float *ms, int32_t *launches);
  * Kernel-level timing (for benchmarks; off by default).  While enabled, the fill
  * launches its kernels one by one instead of replaying a graph, and the runtime
  * records a pair of HIP events with every dispatch, at the kernel's start and end
- * (hipExtLaunchKernelGGL), so a launch's time is the kernel's own.  rk_fill_kernel_stats then reports, for kernel kind `kind`
- * (0 <= kind < *n_kinds), its name as a profiler shows it, the number of its
- * launches in the last solve, their summed device time in milliseconds, the
- * number of candidate evaluations of the recurrence (relaxations, counting
- * only valid (s,t,m,choice) combinations, with k_run option slots per block; see
- * rk_chain_options) those launches performed, and their
- * compulsory table traffic in bytes: every table row a launch reads counted
- * once, its budget columns only, plus every row it writes (and reads back, where
- * it folds into a stored partial).  Any output pointer may be NULL.  Waits for
- * the last solve; timings need profiling to have been on during it.
- * RK_E_INVAL for a kind out of range.
+ * (hipExtLaunchKernelGGL), so a launch's time is the kernel's own.  rk_fill_kernel_stats
+ * then reports, for kernel kind `kind` (0 <= kind < *n_kinds), its name as a profiler
+ * shows it, the number of its launches in the last solve, their summed device time in
+ * milliseconds, and three counts of the last profiled solve:
+ *   - relaxations: candidate evaluations of the recurrence the launches cover (valid
+ *     (s,t,m,choice) combinations, with k_run option slots per block; see
+ *     rk_chain_options);
+ *   - evaluated: those the kernels actually evaluate.  Past the budget msa(s,t) from
+ *     which storing every activation of span (s,t) fits, Opt(s,t,m) is known in closed
+ *     form (the sum of its blocks' cheapest r(F)+r(B), App. C: Opt can never be lower,
+ *     and case 1 with those options reaches it); tiles whose cells all lie there skip;
+ *   - bytes: compulsory table traffic of what runs: every table row a running tile
+ *     reads, counted once over its budget columns, plus every row written (and read
+ *     back where a fold into a stored partial happens).
+ * Any output pointer may be NULL.  Waits for the last solve; timings and the last two
+ * counts need profiling to have been on during it.  RK_E_INVAL for a kind out of range.
  */
 int rk_set_profiling(rk_chain *c, int32_t enable);
 int rk_fill_kernel_stats(rk_chain *c, int32_t kind, int32_t *n_kinds, const char **name,
-                         int32_t *launches, float *total_ms, int64_t *relaxations, int64_t *bytes);
+                         int32_t *launches, float *total_ms, int64_t *relaxations, int64_t *evaluated,
+                         int64_t *bytes);
 
 /*
  * Options the solver evaluates (Sec. 3, Phase 2: the paper's option search returns many

@@ -17,6 +17,7 @@ using rk::DINF;
 struct rk_chain {
     int32_t L = 0, K = 0;
     std::vector<int32_t> x, xbar, c1, need1, P, need2;  // derived per block and option, per split
+    std::vector<int32_t> msa, lb;  // per span row: budget from which storing everything fits, its time
     // Options the kernels evaluate: per block, in the caller's order, the options kept by the
     // dominance test (all of them when pruning is off), padded to k_run slots per block.
     // run_opt maps a slot back to the caller's option index (-1 for padding).  These are the
@@ -27,7 +28,7 @@ struct rk_chain {
     std::vector<int32_t> run_opt, run_xbar, run_c1, run_need1, run_need1max;
 
     int device = -1;
-    void *d_chain = nullptr;  // x | xbar | c1 | need1 | need1max | P | need2 (options: run arrays)
+    void *d_chain = nullptr;  // x | xbar | c1 | need1 | need1max | P | need2 | lb (options: run arrays)
     DevChain dc{};
 
     int32_t max_x = 0;       // largest x_i over the split points i = 1..L-1
@@ -168,8 +169,8 @@ int ensure_device(rk_chain *c)
     }
     build_run(c);
     const int32_t L = c->L, K = c->k_run;
-    const size_t nx = L + 1, nk = (size_t)L * K, nl = (size_t)L * L;
-    const size_t total = nx + 3 * nk + L + 2 * nl;
+    const size_t nx = L + 1, nk = (size_t)L * K, nl = (size_t)L * L, nr = (size_t)rk::n_rows(L);
+    const size_t total = nx + 3 * nk + L + 2 * nl + nr;
     HIPCHK(hipMalloc(&c->d_chain, total * sizeof(int32_t)));
     int32_t *p = static_cast<int32_t *>(c->d_chain);
     size_t off = 0;
@@ -189,11 +190,13 @@ int ensure_device(rk_chain *c)
     c->dc.need1max = put(c->run_need1max);
     c->dc.P = put(c->P);
     c->dc.need2 = put(c->need2);
+    c->dc.lb = put(c->lb);
+    c->dc.h_msa = c->msa.data();
     int64_t xbar_max = 0;
     for (int32_t v : c->run_xbar) xbar_max = std::max<int64_t>(xbar_max, v);
     c->dc.xbar_halo = xbar_max > rk::HMAX ? rk::HMAX + 1 : rk::round64(xbar_max);
     if (!c->dc.x || !c->dc.xbar || !c->dc.c1 || !c->dc.need1 || !c->dc.need1max || !c->dc.P ||
-        !c->dc.need2) {  // leave no half-uploaded arrays behind: the next solve uploads again
+        !c->dc.need2 || !c->dc.lb) {  // leave no half-uploaded arrays behind: the next solve uploads again
         (void)hipFree(c->d_chain);
         c->d_chain = nullptr;
         return RK_E_DEVICE;
@@ -360,6 +363,8 @@ int rk_chain_create(int32_t L, int32_t K, const int32_t *x, const int32_t *fn_ti
         c->kept.assign(nk, 1);
         c->P.assign((size_t)L * L, 0);
         c->need2.assign((size_t)L * L, 0);
+        c->msa.assign((size_t)rk::n_rows(L), 0);
+        c->lb.assign((size_t)rk::n_rows(L), 0);
     } catch (...) {
         delete c;
         return RK_E_NOMEM;
@@ -402,6 +407,33 @@ int rk_chain_create(int32_t L, int32_t K, const int32_t *x, const int32_t *fn_ti
             c->P[(size_t)s * L + i] = (int32_t)p;
             c->need2[(size_t)s * L + i] = (int32_t)std::min(need, kSizeCap);
         }
+    }
+    // Storing everything: every schedule of a span runs each of its blocks' backward once,
+    // paired with one saving forward, so it costs at least lb(s,t) = sum of min_o r(F)+r(B)
+    // (further forwards only add).  Case 1 with a cheapest option at every block reaches lb
+    // as soon as it fits, from msa(s,t) = min over the cheapest options o of block s of
+    // max(need1[s][o], xbar[s][o] + msa(s+1,t)) (msa(s,s): the smallest need1).  Opt being
+    // non-increasing in m, Opt(s,t,m) = lb(s,t) for every m >= msa(s,t).
+    {
+        std::vector<int64_t> cmin(L), prefix(L + 1, 0);
+        for (int32_t s = 0; s < L; ++s) {
+            int64_t v = INT64_MAX;
+            for (int32_t o = 0; o < K; ++o) v = std::min<int64_t>(v, c->c1[(size_t)s * K + o]);
+            cmin[s] = v;
+            prefix[s + 1] = prefix[s] + v;
+        }
+        for (int32_t t = 0; t < L; ++t)
+            for (int32_t s = t; s >= 0; --s) {
+                const int64_t rest = s < t ? c->msa[(size_t)rk::row_of(L, s + 1, t)] : 0;
+                int64_t best = kSizeCap;
+                for (int32_t o = 0; o < K; ++o) {
+                    const size_t j = (size_t)s * K + o;
+                    if (c->c1[j] != cmin[s]) continue;
+                    best = std::min(best, std::max<int64_t>(c->need1[j], s < t ? c->xbar[j] + rest : 0));
+                }
+                c->msa[(size_t)rk::row_of(L, s, t)] = (int32_t)std::min(best, kSizeCap);
+                c->lb[(size_t)rk::row_of(L, s, t)] = (int32_t)(prefix[t + 1] - prefix[s]);
+            }
     }
     for (int32_t i = 1; i < L; ++i) c->max_x = std::max(c->max_x, x[i]);
     *out = c;
@@ -625,7 +657,8 @@ int rk_set_profiling(rk_chain *c, int32_t enable)
 }
 
 int rk_fill_kernel_stats(rk_chain *c, int32_t kind, int32_t *n_kinds, const char **name,
-                         int32_t *launches, float *total_ms, int64_t *relaxations, int64_t *bytes)
+                         int32_t *launches, float *total_ms, int64_t *relaxations, int64_t *evaluated,
+                         int64_t *bytes)
 {
     if (!c) return RK_E_INVAL;
     if (n_kinds) *n_kinds = rk::KFILL_NKINDS;
@@ -647,6 +680,7 @@ int rk_fill_kernel_stats(rk_chain *c, int32_t kind, int32_t *n_kinds, const char
     if (launches) *launches = cnt;
     if (total_ms) *total_ms = sum;
     if (relaxations) *relaxations = c->prof.work[kind];
+    if (evaluated) *evaluated = c->prof.eval[kind];
     if (bytes) *bytes = c->prof.bytes[kind];
     return RK_OK;
 }

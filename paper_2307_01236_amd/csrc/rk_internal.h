@@ -74,6 +74,12 @@ struct DevChain {
     const int32_t *need1max;  // [L] max_o need1[s][o]: every option of block s is valid from here
     const int32_t *P;      // [L*L]  P[s*L+i] = sum_{k=s}^{i-1} r(F_k^0)        (i > s)
     const int32_t *need2;  // [L*L]  smallest m at which the sweep s..i-1 is valid (i > s)
+    // Where storing everything fits (per span row, row_of order): from budget msa on,
+    // Opt(s,t,m) = lb, the sum over the span's blocks of their cheapest r(F)+r(B) (see
+    // rk_chain_create).  msa saturates at 2^30 (far beyond any budget column); the host
+    // uses it to size each launch.
+    const int32_t *lb;     // [L(L+1)/2]
+    const int32_t *h_msa;  // [L(L+1)/2], host memory
     int32_t xbar_halo;     // round64(max xbar): how far left case 1 reads from column m
 };
 
@@ -105,8 +111,9 @@ struct Profiler {
     std::vector<hipEvent_t> events;  // pool, 2 per launch
     std::vector<int32_t> kinds;      // kernel kind of each bracketed launch
     int32_t n = 0;                   // launches bracketed in the current solve
-    int64_t work[8] = {};            // relaxations per kernel kind in the current solve
-    int64_t bytes[8] = {};           // compulsory table traffic per kernel kind
+    int64_t work[8] = {};            // relaxations of the recurrence per kernel kind in the current solve
+    int64_t eval[8] = {};            // relaxations evaluated (tiles past msa skip); profiling only
+    int64_t bytes[8] = {};           // compulsory table traffic of what runs; profiling only
     // two events from the pool for the next launch, which is of kind `kind`
     hipError_t slot(int32_t kind, hipEvent_t *start, hipEvent_t *stop);
     void reset(hipStream_t s)
@@ -115,6 +122,7 @@ struct Profiler {
         n = 0;
         kinds.clear();
         for (int64_t &w : work) w = 0;
+        for (int64_t &w : eval) w = 0;
         for (int64_t &b : bytes) b = 0;
     }
 };

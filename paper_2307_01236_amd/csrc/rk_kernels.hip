@@ -16,6 +16,7 @@
 
 #include <hip/hip_ext.h>
 
+#include <algorithm>
 #include <type_traits>
 
 namespace rk {
@@ -88,15 +89,25 @@ constexpr uint32_t OOB = 0x80000000u;
 
 // ---------------------------------------------------------------------------------------
 // Workgroups of a launch go to the 8 XCDs round-robin (id g to XCD g mod 8), and each XCD
-// has its own L2.  Renumbering them so that every XCD gets one contiguous range of logical
-// tiles puts tiles that share operand rows into the same L2 at about the same time.
-// A bijection of [0, G); correctness does not depend on the dispatch order.
+// has its own L2.  Tiles are laid out as column chunks x n_idx tiles per chunk, and XCD x
+// (g mod 8) takes the chunks x, x + 8, x + 16, ..., each with its n_idx tiles in order.
+// Every XCD then keeps whole column chunks (tiles that share operand rows share its L2, at
+// about the same time) and gets chunks from the whole budget range, so work that shrinks
+// with the budget column (tiles past the store-everything budget) stays even over the
+// XCDs.  Launches hold 8 ceil(n_chunks / 8) n_idx workgroups; *chunk >= n_chunks marks a
+// spare one.  Correctness does not depend on the dispatch order.
 // ---------------------------------------------------------------------------------------
-__device__ inline uint32_t xcd_tile(uint32_t g, uint32_t G)
+__device__ inline void chunk_tile(uint32_t g, uint32_t n_idx, int32_t *chunk, int32_t *idx)
 {
-    constexpr uint32_t NX = 8;
-    const uint32_t x = g % NX, j = g / NX, base = G / NX, rem = G % NX;
-    return (x < rem ? x * (base + 1) : rem * (base + 1) + (x - rem) * base) + j;
+    const uint32_t j = g / 8;
+    // scalars: the division is expanded with vector instructions, and without the hint
+    // every address derived from the tile would be computed (and loaded) per lane
+    *chunk = __builtin_amdgcn_readfirstlane((int32_t)(g % 8 + 8 * (j / n_idx)));
+    *idx = __builtin_amdgcn_readfirstlane((int32_t)(j % n_idx));
+}
+static inline uint32_t chunk_grid(int32_t n_chunks, int32_t n_idx)
+{
+    return (uint32_t)(8 * ((n_chunks + 7) / 8) * n_idx);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -133,7 +144,7 @@ __device__ inline uint32_t buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uin
 }
 
 template <int SR, int TW, int TH, int NW>
-__global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int32_t tau)
+__global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int32_t tau, int32_t n_chunks)
 {
     // TH waves share SR rows, each keeping TW of the T = TW TH ends of those rows
     constexpr int T = TW * TH, SW = SR * NW / TH, CI = PROD_CI;
@@ -153,9 +164,11 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
     const int32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int32_t s_end = L - tau;  // rows that own at least one cell of the band
     const uint32_t n_rb = (uint32_t)(s_end + SW - 1) / SW;
-    const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);  // row blocks of a column chunk adjacent
-    const int32_t S0 = (int32_t)(tile % n_rb) * SW;
-    const uint32_t mchunk = tile / n_rb;
+    int32_t chunk, rb;  // row blocks of a column chunk adjacent, chunks spread over the XCDs
+    chunk_tile(blockIdx.x, n_rb, &chunk, &rb);
+    if (chunk >= n_chunks) return;
+    const int32_t S0 = rb * SW;
+    const uint32_t mchunk = (uint32_t)chunk;
     const int32_t rg = wave / TH, kh = (wave % TH) * TW;  // row group, first end offset
     const int32_t s0 = S0 + rg * SR;
     const int64_t stride = tb.stride;
@@ -167,6 +180,7 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
     const int32_t *const ap_end = tb.ap + (tb.inf_row + 1 + SLACK) * stride;
     const int32_t t0 = S0 + tau;  // first end the workgroup covers
     const int32_t i_lo = S0 + 1, i_hi = min(S0 + SW - 1 + tau, L - 1);
+
 
     // right operands: this wave stages ends t0 + wave + NW*jj, which for one split i are
     // rows (i, t0) + wave + NW*jj (the spans starting at i are consecutive rows)
@@ -536,22 +550,19 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
 // on one XCD: each XCD keeps the same range of columns as in the finalize launches, whose
 // recent rows the mids read.
 template <int WD, bool LO0>
-__global__ __launch_bounds__(64) void k_mid(DevChain ch, Tables tb, int32_t tau, int32_t accumulate)
+__global__ __launch_bounds__(64) void k_mid(DevChain ch, Tables tb, int32_t tau, int32_t accumulate,
+                                            int32_t n_chunks)
 {
     constexpr int R = mid_rows<WD>();
     const int32_t n_blk = (ch.L - tau + R - 1) / R;
-    const int32_t per_group = n_blk * ((tb.W + 63) / 64);
-    const int32_t g = (int32_t)xcd_tile(blockIdx.x, gridDim.x);
-    if (LO0) {
-        if (g < per_group) mid_tile<WD, true, LO0>(ch, tb, tau, accumulate, g);
-    } else {
-        // column chunk mc, then group A's n_blk tiles and group B's; gi indexes the group
-        const int32_t mc = g / (2 * n_blk), rem = g % (2 * n_blk), gi = mc * n_blk + rem % n_blk;
-        if (mc * n_blk < per_group) {
-            if (rem < n_blk) mid_tile<WD, true, false>(ch, tb, tau, accumulate, gi);
-            else mid_tile<WD, false, false>(ch, tb, tau, accumulate, gi);
-        }
-    }
+    // per column chunk: group A's n_blk tiles, then group B's (lo > 0); gi indexes the group
+    int32_t mc, rem;
+    chunk_tile(blockIdx.x, (LO0 ? 1 : 2) * n_blk, &mc, &rem);
+    if (mc >= n_chunks) return;
+    const int32_t gi = mc * n_blk + rem % n_blk;
+    if (LO0) mid_tile<WD, true, LO0>(ch, tb, tau, accumulate, gi);
+    else if (rem < n_blk) mid_tile<WD, true, false>(ch, tb, tau, accumulate, gi);
+    else mid_tile<WD, false, false>(ch, tb, tau, accumulate, gi);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -583,7 +594,8 @@ __device__ inline int32_t ldrow(const int32_t *base, uint32_t pitch, uint32_t by
     return __builtin_amdgcn_raw_buffer_load_b32(r, (int)byte_off, 0, 0);
 }
 
-__global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t d, int32_t midmin)
+__global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t d, int32_t midmin,
+                                                 int32_t n_chunks, int32_t n_run)
 {
     constexpr int32_t FB = 8, NC = FC / FT, NST = (HMAX + FC) / FT;
     __shared__ int32_t seg[HMAX + FC];
@@ -592,9 +604,11 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
     // case-1 row (s+1, t) of a cell was written in the previous launch by the workgroup of
     // the neighbouring tile, so it is often still in that XCD's L2 (rows adjacent: 5.95 ms a
     // fill, column chunks adjacent: 6.15 ms, no XCD-aware order: 6.7 ms).
-    const uint32_t tile = xcd_tile(blockIdx.x, gridDim.x);
-    const int32_t s = (int32_t)(tile % (uint32_t)(L - d)), t = s + d;
-    const int32_t mbase = (int32_t)(tile / (uint32_t)(L - d)) * FC;
+    int32_t chunk, s;
+    chunk_tile(blockIdx.x, (uint32_t)(L - d), &chunk, &s);
+    if (chunk >= n_chunks) return;
+    const int32_t t = s + d;
+    const int32_t mbase = chunk * FC;
     const int32_t lane = (int32_t)(threadIdx.x & 63);
     const int32_t wave = __builtin_amdgcn_readfirstlane((int32_t)(threadIdx.x >> 6));
     const int32_t m0 = mbase + 64 * NC * wave;  // the wave's first column
@@ -604,109 +618,120 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
     const int32_t padl = tb.padl;
     int32_t *const orow = tb.opt + row_of(L, s, t) * stride + padl;  // column 0
     const int32_t D = (d / midmin) * midmin;  // the products cover splits with max(a, b) < D
-
-    // case-1 row, staged: column mbase - H + q at seg[q]
-    const int32_t H = ch.xbar_halo;
-    const bool staged = d > 0 && H <= HMAX;
-    const int32_t *const rest = d > 0 ? tb.opt + row_of(L, s + 1, t) * stride + padl : nullptr;
-    int32_t stv[NST];
-    if (staged) {
-#pragma unroll
-        for (int k = 0; k < NST; ++k) {
-            const int32_t q = (int32_t)threadIdx.x + FT * k, c = mbase - H + q;
-            stv[k] = q < H + FC && c >= -padl ? rest[c] : DINF;
-        }
-    }
-
-    // per-lane column offsets (past the last budget: the last one, computed and not stored)
-    uint32_t col[NC];  // byte offsets
-#pragma unroll
-    for (int c = 0; c < NC; ++c) col[c] = (uint32_t)min(ml + 64 * c, W - 1) * 4u;
+    int32_t *const arow = tb.ap + row_of(L, s, t) * stride + padl;
+    const int32_t ip = t + 1 < L ? s * L + t + 1 : 0;
+    // From budget msa(s,t) on, storing everything fits and Opt(s,t,m) = lb(s,t).  Chunks from
+    // n_run on lie past the msa of every cell of the diagonal (the host's bound): they only
+    // store.  The products and mids of these spans ran on at least the chunks below n_run.
+    // (The stores stay after every load on both paths, so the loads of the per-block and
+    // per-option arrays may use the scalar cache.)
     int32_t best[NC];
+    if (chunk >= n_run) {
+        const int32_t lbv = ch.lb[row_of(L, s, t)];
 #pragma unroll
-    for (int c = 0; c < NC; ++c) best[c] = D > 0 ? ldb(orow, col[c]) : DINF;
+        for (int c = 0; c < NC; ++c) best[c] = lbv;
+    } else {
 
-    // splits i0 .. i0+n-1: ap(s, i-1) + Opt(i, t, m - x_i).  Pointers at column 0:
-    // ap row (s, i-1) is i-1-s rows after (s, s); Opt row (i+1, t) is L-1-i rows after (i, t)
-    auto splits = [&](int32_t i0, int32_t n) {
-        const int32_t *pa = tb.ap + (row_of(L, s, s) + (i0 - 1 - s)) * stride + padl;
-        const int32_t *pq = tb.opt + row_of(L, i0, t) * stride + padl;
-        int32_t i = i0;
-        for (int32_t j0 = 0; j0 < n; j0 += FB) {
-            int32_t va[FB][NC], vq[FB][NC];
+        // case-1 row, staged: column mbase - H + q at seg[q]
+        const int32_t H = ch.xbar_halo;
+        const bool staged = d > 0 && H <= HMAX;
+        const int32_t *const rest = d > 0 ? tb.opt + row_of(L, s + 1, t) * stride + padl : nullptr;
+        int32_t stv[NST];
+        if (staged) {
 #pragma unroll
-            for (int u = 0; u < FB; ++u) {
-                if (j0 + u < n) {
-                    // a shift x_i > padl happens only when padl >= W: the read lands in the left pad
-                    const int32_t *const q = pq - min(ch.x[i], padl);
+            for (int k = 0; k < NST; ++k) {
+                const int32_t q = (int32_t)threadIdx.x + FT * k, c = mbase - H + q;
+                stv[k] = q < H + FC && c >= -padl ? rest[c] : DINF;
+            }
+        }
+
+        // per-lane column offsets (past the last budget: the last one, computed and not stored)
+        uint32_t col[NC];  // byte offsets
 #pragma unroll
-                    for (int c = 0; c < NC; ++c) {
-                        va[u][c] = ldrow(pa, pitch, col[c]);
-                        vq[u][c] = ldrow(q, pitch, col[c]);
-                    }
-                    pa += stride;
-                    pq += (int64_t)(L - 1 - i) * stride;
-                    ++i;
-                } else {
+        for (int c = 0; c < NC; ++c) col[c] = (uint32_t)min(ml + 64 * c, W - 1) * 4u;
 #pragma unroll
-                    for (int c = 0; c < NC; ++c) {
-                        va[u][c] = DINF;
-                        vq[u][c] = 0;
+        for (int c = 0; c < NC; ++c) best[c] = D > 0 ? ldb(orow, col[c]) : DINF;
+
+        // splits i0 .. i0+n-1: ap(s, i-1) + Opt(i, t, m - x_i).  Pointers at column 0:
+        // ap row (s, i-1) is i-1-s rows after (s, s); Opt row (i+1, t) is L-1-i rows after (i, t)
+        auto splits = [&](int32_t i0, int32_t n) {
+            const int32_t *pa = tb.ap + (row_of(L, s, s) + (i0 - 1 - s)) * stride + padl;
+            const int32_t *pq = tb.opt + row_of(L, i0, t) * stride + padl;
+            int32_t i = i0;
+            for (int32_t j0 = 0; j0 < n; j0 += FB) {
+                int32_t va[FB][NC], vq[FB][NC];
+#pragma unroll
+                for (int u = 0; u < FB; ++u) {
+                    if (j0 + u < n) {
+                        // a shift x_i > padl happens only when padl >= W: the read lands in the left pad
+                        const int32_t *const q = pq - min(ch.x[i], padl);
+#pragma unroll
+                        for (int c = 0; c < NC; ++c) {
+                            va[u][c] = ldrow(pa, pitch, col[c]);
+                            vq[u][c] = ldrow(q, pitch, col[c]);
+                        }
+                        pa += stride;
+                        pq += (int64_t)(L - 1 - i) * stride;
+                        ++i;
+                    } else {
+#pragma unroll
+                        for (int c = 0; c < NC; ++c) {
+                            va[u][c] = DINF;
+                            vq[u][c] = 0;
+                        }
                     }
                 }
+#pragma unroll
+                for (int u = 0; u < FB; ++u)
+#pragma unroll
+                    for (int c = 0; c < NC; ++c) best[c] = min(best[c], va[u][c] + vq[u][c]);
             }
-#pragma unroll
-            for (int u = 0; u < FB; ++u)
-#pragma unroll
-                for (int c = 0; c < NC; ++c) best[c] = min(best[c], va[u][c] + vq[u][c]);
-        }
-    };
-    if (D == 0) {
-        splits(s + 1, d);
-    } else {
-        splits(s + 1, d - D);      // t - i >= D
-        splits(s + D + 1, d - D);  // i - 1 - s >= D
-    }
-
-    // case 1, option o: r(F_s^o) + r(B_s^o) + Opt(s+1,t,m-xbar), valid iff m >= need1[s][o]
-    const int32_t *const c1 = ch.c1 + s * K, *const need1 = ch.need1 + s * K, *const xbar = ch.xbar + s * K;
-    if (d == 0) {
-        for (int32_t o = 0; o < K; ++o)
-#pragma unroll
-            for (int c = 0; c < NC; ++c)
-                if (ml + 64 * c >= need1[o]) best[c] = min(best[c], c1[o]);
-    } else if (staged) {
-#pragma unroll
-        for (int k = 0; k < NST; ++k) {
-            const int32_t q = (int32_t)threadIdx.x + FT * k;
-            if (q < H + FC) seg[q] = stv[k];
-        }
-        __syncthreads();
-        const int32_t *const sg = seg + H + (ml - mbase);  // column ml
-        if (m0 >= ch.need1max[s]) {
-            for (int32_t o = 0; o < K; ++o) {
-                const int32_t *const so = sg - xbar[o];
-#pragma unroll
-                for (int c = 0; c < NC; ++c) best[c] = min(best[c], c1[o] + so[64 * c]);
-            }
+        };
+        if (D == 0) {
+            splits(s + 1, d);
         } else {
-            for (int32_t o = 0; o < K; ++o) {
-                const int32_t *const so = sg - xbar[o];
+            splits(s + 1, d - D);      // t - i >= D
+            splits(s + D + 1, d - D);  // i - 1 - s >= D
+        }
+
+        // case 1, option o: r(F_s^o) + r(B_s^o) + Opt(s+1,t,m-xbar), valid iff m >= need1[s][o]
+        const int32_t *const c1 = ch.c1 + s * K, *const need1 = ch.need1 + s * K, *const xbar = ch.xbar + s * K;
+        if (d == 0) {
+            for (int32_t o = 0; o < K; ++o)
 #pragma unroll
                 for (int c = 0; c < NC; ++c)
-                    if (ml + 64 * c >= need1[o]) best[c] = min(best[c], c1[o] + so[64 * c]);
-            }
-        }
-    } else {
-        for (int32_t o = 0; o < K; ++o)
+                    if (ml + 64 * c >= need1[o]) best[c] = min(best[c], c1[o]);
+        } else if (staged) {
 #pragma unroll
-            for (int c = 0; c < NC; ++c)
-                if (ml + 64 * c >= need1[o]) best[c] = min(best[c], c1[o] + ldb(rest - xbar[o], col[c]));
+            for (int k = 0; k < NST; ++k) {
+                const int32_t q = (int32_t)threadIdx.x + FT * k;
+                if (q < H + FC) seg[q] = stv[k];
+            }
+            __syncthreads();
+            const int32_t *const sg = seg + H + (ml - mbase);  // column ml
+            if (m0 >= ch.need1max[s]) {
+                for (int32_t o = 0; o < K; ++o) {
+                    const int32_t *const so = sg - xbar[o];
+#pragma unroll
+                    for (int c = 0; c < NC; ++c) best[c] = min(best[c], c1[o] + so[64 * c]);
+                }
+            } else {
+                for (int32_t o = 0; o < K; ++o) {
+                    const int32_t *const so = sg - xbar[o];
+#pragma unroll
+                    for (int c = 0; c < NC; ++c)
+                        if (ml + 64 * c >= need1[o]) best[c] = min(best[c], c1[o] + so[64 * c]);
+                }
+            }
+        } else {
+            for (int32_t o = 0; o < K; ++o)
+#pragma unroll
+                for (int c = 0; c < NC; ++c)
+                    if (ml + 64 * c >= need1[o]) best[c] = min(best[c], c1[o] + ldb(rest - xbar[o], col[c]));
+        }
     }
 
     // stores last: until here every scalar operand may come from the scalar cache
-    int32_t *const arow = tb.ap + row_of(L, s, t) * stride + padl;
-    const int32_t ip = t + 1 < L ? s * L + t + 1 : 0;
     const int32_t need2 = t + 1 < L ? ch.need2[ip] : 0, P = t + 1 < L ? ch.P[ip] : 0;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
@@ -734,54 +759,92 @@ static int64_t product_work(int32_t L, int32_t W, int32_t tau, int32_t T, int32_
     return n * W;
 }
 
-// Compulsory table traffic of a product launch: the distinct ap rows (s, s+a) and Opt rows
-// (t-b, t) that some real candidate reads, plus the target rows written (and read back when
-// folding into a stored partial); W int32 per row.  Per row s (per end t) the spans a (b)
-// with a real candidate form one interval, the union over the target spans.
-static int64_t product_bytes(int32_t L, int32_t W, int32_t tau, int32_t T, int32_t alo, int32_t ahi,
-                             int32_t blo, int32_t bhi, bool accumulate)
+// What a product launch does when it runs only some column chunks: chunks(s, t) = how many
+// 64-column chunks of cell (s,t)'s tile run.  Adds the relaxations evaluated and the
+// compulsory table traffic of the running tiles: per run of chunks with the same running tiles, the
+// distinct ap rows (s, s+a) and Opt rows (t-b, t) some real candidate of a running cell
+// reads, plus the target rows written (and read back when folding into a stored partial).
+template <class F>
+static void product_account(int32_t L, int32_t W, int32_t tau, int32_t T, int32_t alo, int32_t ahi,
+                            int32_t blo, int32_t bhi, bool accumulate, F chunks, int64_t *work, int64_t *bytes)
 {
-    int64_t rows = 0;
-    for (int32_t s = 0; s < L - tau; ++s) {
-        int32_t lo = 0x7fffffff, hi = -1;
-        for (int32_t dd = tau; dd < min(tau + T, L - s); ++dd) {
-            const int32_t a0 = max(alo, dd - bhi), a1 = min(ahi - 1, dd - 1 - blo);
-            if (a0 <= a1) lo = min(lo, a0), hi = max(hi, a1);
+    const int32_t n_mc = (W + 63) / 64, dmax = min(tau + T, L);
+    std::vector<int32_t> cuts{0};
+    for (int32_t dd = tau; dd < dmax; ++dd) {
+        int64_t c = 0;  // real splits of a cell of span dd
+        for (int32_t a = alo; a < min(ahi, dd); ++a) c += (dd - 1 - a >= blo && dd - 1 - a < bhi);
+        for (int32_t s = 0; s + dd < L; ++s) {
+            const int32_t k = min(chunks(s, s + dd), n_mc);
+            *work += c * min(W, 64 * k);
+            cuts.push_back(k);
         }
-        if (hi >= lo) rows += hi - lo + 1;
     }
-    for (int32_t t = tau; t < L; ++t) {
-        int32_t lo = 0x7fffffff, hi = -1;
-        for (int32_t dd = tau; dd < min(tau + T, t + 1); ++dd) {
-            const int32_t b0 = max(blo, dd - ahi), b1 = min(bhi - 1, dd - 1 - alo);
-            if (b0 <= b1) lo = min(lo, b0), hi = max(hi, b1);
+    std::sort(cuts.begin(), cuts.end());
+    cuts.erase(std::unique(cuts.begin(), cuts.end()), cuts.end());
+    for (size_t j = 1; j < cuts.size(); ++j) {
+        const int32_t c0 = cuts[j - 1], c1 = cuts[j];  // chunks [c0, c1) run the cells with chunks >= c1
+        const int64_t cols = min(W, 64 * c1) - 64 * c0;
+        if (cols <= 0) continue;
+        int64_t rows = 0;
+        for (int32_t s = 0; s < L - tau; ++s) {
+            int32_t lo = 0x7fffffff, hi = -1;
+            for (int32_t dd = tau; dd < min(dmax, L - s); ++dd) {
+                if (min(chunks(s, s + dd), n_mc) < c1) continue;
+                const int32_t a0 = max(alo, dd - bhi), a1 = min(ahi - 1, dd - 1 - blo);
+                if (a0 <= a1) lo = min(lo, a0), hi = max(hi, a1);
+                rows += accumulate ? 2 : 1;  // the target row written (and read back)
+            }
+            if (hi >= lo) rows += hi - lo + 1;
         }
-        if (hi >= lo) rows += hi - lo + 1;
+        for (int32_t t = tau; t < L; ++t) {
+            int32_t lo = 0x7fffffff, hi = -1;
+            for (int32_t dd = tau; dd < min(dmax, t + 1); ++dd) {
+                if (min(chunks(t - dd, t), n_mc) < c1) continue;
+                const int32_t b0 = max(blo, dd - ahi), b1 = min(bhi - 1, dd - 1 - alo);
+                if (b0 <= b1) lo = min(lo, b0), hi = max(hi, b1);
+            }
+            if (hi >= lo) rows += hi - lo + 1;
+        }
+        *bytes += rows * cols * 4;
     }
-    int64_t cells = 0;
-    for (int32_t dd = tau; dd < min(tau + T, L); ++dd) cells += L - dd;
-    return (rows + cells * (accumulate ? 2 : 1)) * W * 4;
 }
+
+// 64-column chunks a product or mid launch runs when its target cells' largest msa is sat:
+// whole finalize workgroups (FC = 128 columns), so that every column a finalize computes
+// from operands has its partial.
+static inline int32_t run_chunks(int32_t sat) { return (int32_t)(((int64_t)sat + 127) / 128 * 2); }
 
 template <int WD>
 static hipError_t launch_mid(const DevChain &ch, const Tables &tb, hipStream_t stream, int32_t d,
                              int32_t *n, Profiler *prof)
 {
     hipError_t e;
-    const int32_t lo = d - WD;
+    const int32_t lo = d - WD, L = ch.L;
     constexpr int R = mid_rows<WD>();
-    const int32_t n_blk = (ch.L - d + R - 1) / R, n_mc = (tb.W + 63) / 64;
-    const dim3 grid((lo == 0 ? 1 : 2) * n_blk * n_mc);
-    e = lo == 0 ? launch(prof, KFILL_MID, k_mid<WD, true>, grid, dim3(64), stream, ch, tb, d, 0)
-                : launch(prof, KFILL_MID, k_mid<WD, false>, grid, dim3(64), stream, ch, tb, d, 1);
+    const int32_t n_blk = (L - d + R - 1) / R, n_mc = (tb.W + 63) / 64;
+    // column chunks below the largest msa of the target spans [d, d + WD) (msa grows with t)
+    int32_t sat = 0;
+    for (int32_t s = 0; s < L - d; ++s) sat = max(sat, ch.h_msa[row_of(L, s, min(s + d + WD - 1, L - 1))]);
+    const int32_t n_chunks = min(n_mc, run_chunks(sat));
+    prof->work[KFILL_MID] += lo == 0 ? product_work(L, tb.W, d, WD, 0, WD, 0, WD)
+                                     : product_work(L, tb.W, d, WD, lo, d, 0, d) +
+                                           product_work(L, tb.W, d, WD, 0, lo, lo, d);
+    if (n_chunks == 0) return hipSuccess;  // every target cell is past msa: the finalize stores it
+    const dim3 grid(chunk_grid(n_chunks, (lo == 0 ? 1 : 2) * n_blk));
+    e = lo == 0 ? launch(prof, KFILL_MID, k_mid<WD, true>, grid, dim3(64), stream, ch, tb, d, 0, n_chunks)
+                : launch(prof, KFILL_MID, k_mid<WD, false>, grid, dim3(64), stream, ch, tb, d, 1, n_chunks);
     if (e != hipSuccess) return e;
     ++*n;
-    prof->work[KFILL_MID] += lo == 0 ? product_work(ch.L, tb.W, d, WD, 0, WD, 0, WD)
-                                     : product_work(ch.L, tb.W, d, WD, lo, d, 0, d) +
-                                           product_work(ch.L, tb.W, d, WD, 0, lo, lo, d);
-    prof->bytes[KFILL_MID] += lo == 0 ? product_bytes(ch.L, tb.W, d, WD, 0, WD, 0, WD, false)
-                                      : product_bytes(ch.L, tb.W, d, WD, lo, d, 0, d, true) +
-                                            product_bytes(ch.L, tb.W, d, WD, 0, lo, lo, d, true);
+    if (prof->on) {  // what runs: every tile on the launch's first n_chunks column chunks
+        auto run = [&](int32_t, int32_t) { return n_chunks; };
+        int64_t *w = &prof->eval[KFILL_MID], *by = &prof->bytes[KFILL_MID];
+        if (lo == 0) {
+            product_account(L, tb.W, d, WD, 0, WD, 0, WD, false, run, w, by);
+        } else {
+            product_account(L, tb.W, d, WD, lo, d, 0, d, true, run, w, by);
+            product_account(L, tb.W, d, WD, 0, lo, lo, d, true, run, w, by);
+        }
+    }
     return hipSuccess;
 }
 
@@ -802,12 +865,24 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
     for (int32_t d = 0; d < ch.L; ++d) {
         if (d > 0 && d % BAND == 0) {
             constexpr int SR = 4, TW = 16, TH = 2, NW = 4, SW = SR * NW / TH;  // product tile
-            const dim3 grid(((tb.W + 63) / 64) * ((ch.L - d + SW - 1) / SW));
-            e = launch(prof, KFILL_PRODUCT, k_product<SR, TW, TH, NW>, grid, dim3(NW * 64), stream, ch, tb, d);
-            if (e != hipSuccess) return e;
-            ++n;
+            int32_t sat = 0;  // column chunks below the largest msa of the band's spans
+            for (int32_t s = 0; s < ch.L - d; ++s)
+                sat = max(sat, ch.h_msa[row_of(ch.L, s, min(s + d + BAND - 1, ch.L - 1))]);
+            const int32_t n_chunks = min((tb.W + 63) / 64, run_chunks(sat));
             prof->work[KFILL_PRODUCT] += product_work(ch.L, tb.W, d, BAND, 0, d, 0, d);
-            prof->bytes[KFILL_PRODUCT] += product_bytes(ch.L, tb.W, d, BAND, 0, d, 0, d, false);
+            if (n_chunks > 0) {
+                const dim3 grid(chunk_grid(n_chunks, (ch.L - d + SW - 1) / SW));
+                e = launch(prof, KFILL_PRODUCT, k_product<SR, TW, TH, NW>, grid, dim3(NW * 64), stream, ch, tb, d,
+                           n_chunks);
+                if (e != hipSuccess) return e;
+                ++n;
+            }
+            if (prof->on) {  // every tile on the launch's first n_chunks column chunks
+                const int32_t L = ch.L;
+                auto tile = [&](int32_t, int32_t) { return n_chunks; };
+                product_account(L, tb.W, d, BAND, 0, d, 0, d, false, tile, &prof->eval[KFILL_PRODUCT],
+                                &prof->bytes[KFILL_PRODUCT]);
+            }
         } else if (d % 16 == 0 && d > 0) {
             if ((e = launch_mid<16>(ch, tb, stream, d, &n, prof)) != hipSuccess) return e;
         } else if (d % 8 == 0 && d > 0) {
@@ -815,16 +890,26 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
         } else if (d % 4 == 0 && d > 0 && midmin == 4) {
             if ((e = launch_mid<4>(ch, tb, stream, d, &n, prof)) != hipSuccess) return e;
         }
-        e = launch(prof, KFILL_FINALIZE, k_finalize, dim3(fin_x * (ch.L - d)), dim3(FT), stream, ch, tb, d,
-                   midmin);
+        int32_t sat = 0;  // chunks from n_run on lie past every cell's msa: they only store
+        for (int32_t s = 0; s + d < ch.L; ++s) sat = max(sat, ch.h_msa[row_of(ch.L, s, s + d)]);
+        const int32_t n_run = (int32_t)std::min<int64_t>(fin_x, ((int64_t)sat + FC - 1) / FC);
+        e = launch(prof, KFILL_FINALIZE, k_finalize, dim3(chunk_grid(fin_x, ch.L - d)), dim3(FT), stream, ch, tb, d,
+                   midmin, fin_x, n_run);
         if (e != hipSuccess) return e;
         ++n;
         const int32_t D = (d / midmin) * midmin, near = D > 0 ? 2 * (d - D) : d;
         prof->work[KFILL_FINALIZE] += (int64_t)(ch.L - d) * (near + ch.K) * tb.W;
-        // per cell: two operand rows per split, the stored partial, the case-1 row, the Opt
-        // row written; the ap row written where a later split uses it
-        prof->bytes[KFILL_FINALIZE] +=
-            ((int64_t)(ch.L - d) * (2 * near + (D > 0) + (d > 0) + 1) + (ch.L - d - 1)) * tb.W * 4;
+        if (prof->on) {
+            // per cell, in the workgroups below msa: two operand rows per split, the stored
+            // partial, the case-1 row, the Opt row written; past msa only the Opt row
+            // written; the ap row written where a later split uses it
+            for (int32_t s = 0; s + d < ch.L; ++s) {
+                const int64_t run = std::min<int64_t>(tb.W, (int64_t)n_run * FC);
+                prof->eval[KFILL_FINALIZE] += run * (near + ch.K);
+                prof->bytes[KFILL_FINALIZE] +=
+                    (run * (2 * near + (D > 0) + (d > 0) + 1) + (tb.W - run) + (s + d + 1 < ch.L ? tb.W : 0)) * 4;
+            }
+        }
     }
     *launches = n;
     return hipSuccess;

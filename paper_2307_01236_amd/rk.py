@@ -71,7 +71,7 @@ def load():
         lib.rk_set_option_pruning.argtypes = [C.c_void_p, i32]
         lib.rk_chain_options.argtypes = [C.c_void_p, i32p, i32p]
         lib.rk_fill_kernel_stats.argtypes = [C.c_void_p, i32, i32p, P(C.c_char_p), i32p,
-                                             P(C.c_float), P(i64), P(i64)]
+                                             P(C.c_float), P(i64), P(i64), P(i64)]
         lib.rk_strerror.argtypes = [C.c_int]
         lib.rk_strerror.restype = C.c_char_p
         for n in EXPORTS:
@@ -190,17 +190,18 @@ def rk_set_profiling(h, enable: bool) -> None:
 
 
 def rk_fill_kernel_stats(h):
-    """{kernel name: (launches, summed device ms, relaxations, compulsory bytes)} for the
-    last solve."""
+    """{kernel name: (launches, summed device ms, relaxations of the recurrence, relaxations
+    evaluated, compulsory bytes)} for the last solve."""
     lib = load()
     nk = C.c_int32(0)
-    lib.rk_fill_kernel_stats(h, -1, C.byref(nk), None, None, None, None, None)
+    lib.rk_fill_kernel_stats(h, -1, C.byref(nk), None, None, None, None, None, None)
     out = {}
     for k in range(nk.value):
-        name, n, ms, w, b = C.c_char_p(), C.c_int32(0), C.c_float(0), C.c_int64(0), C.c_int64(0)
+        name, n, ms = C.c_char_p(), C.c_int32(0), C.c_float(0)
+        w, e, b = C.c_int64(0), C.c_int64(0), C.c_int64(0)
         _check(lib.rk_fill_kernel_stats(h, k, None, C.byref(name), C.byref(n), C.byref(ms),
-                                        C.byref(w), C.byref(b)), "rk_fill_kernel_stats")
-        out[name.value.decode()] = (int(n.value), float(ms.value), int(w.value), int(b.value))
+                                        C.byref(w), C.byref(e), C.byref(b)), "rk_fill_kernel_stats")
+        out[name.value.decode()] = (int(n.value), float(ms.value), int(w.value), int(e.value), int(b.value))
     return out
 
 
