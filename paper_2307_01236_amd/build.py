@@ -11,7 +11,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "librkrotor.so")
-SOURCES = ["rk_api.hip", "rk_kernels.hip"]
+SOURCES = ["rk_api.hip", "rk_kernels.hip", "rk_host.cpp"]
 CALIB_LIB = os.path.join(PKG, "librkcalib.so")
 CALIB_SOURCES = ["rk_calib.hip"]
 ARCH = "gfx950"

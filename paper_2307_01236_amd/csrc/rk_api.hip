@@ -9,29 +9,23 @@
 #include <new>
 #include <vector>
 
+#include "rk_host.h"
 #include "rk_internal.h"
 
 using rk::DevChain;
 using rk::DINF;
 
 struct rk_chain {
-    int32_t L = 0, K = 0;
-    std::vector<int32_t> x, xbar, c1, need1, P, need2;  // derived per block and option, per split
-    std::vector<int32_t> msa, lb;  // per span row: budget from which storing everything fits, its time
-    // Options the kernels evaluate: per block, in the caller's order, the options kept by the
-    // dominance test (all of them when pruning is off), padded to k_run slots per block.
-    // run_opt maps a slot back to the caller's option index (-1 for padding).  These are the
-    // arrays on the device; run_prune is the setting they were built with.
-    std::vector<uint8_t> kept;  // [L*K] option survives the dominance test
+    rk::HostChain h;  // the caller's chain and everything derived from it on the host
+    // Options the kernels evaluate (rk::host_run_slots): built with the pruning setting
+    // run_prune from version run_version of the host data (bumped when it changes).
     bool prune = true, run_prune = true;
-    int32_t k_run = 0;
-    std::vector<int32_t> run_opt, run_xbar, run_c1, run_need1, run_need1max;
+    int64_t host_version = 0, run_version = -1;
+    rk::RunSlots run;
 
     int device = -1;
-    void *d_chain = nullptr;  // x | xbar | c1 | need1 | need1max | P | need2 | lb (options: run arrays)
+    void *d_chain = nullptr;  // x | xbar | c1 | need1 | need1max | P | need2 | lb (options: run slots)
     DevChain dc{};
-
-    int32_t max_x = 0;       // largest x_i over the split points i = 1..L-1
 
     void *own_ws = nullptr;  // tables owned by the chain (rk_solve)
     size_t own_ws_bytes = 0;
@@ -64,8 +58,6 @@ struct rk_chain {
 };
 
 namespace {
-
-constexpr int64_t kSizeCap = int64_t(1) << 30;  // derived sizes saturate here (above any budget)
 
 #define HIPCHK(expr)                                    \
     do {                                                \
@@ -100,64 +92,24 @@ int geometry(const rk_chain *c, int32_t M, Geometry *g, size_t *bytes)
 {
     if (M < 0 || M > RK_MAX_M) return RK_E_INVAL;
     g->W = M + 1;
-    g->padl = rk::round64(std::min<int64_t>(c->max_x, g->W));
+    g->padl = rk::round64(std::min<int64_t>(c->h.max_x, g->W));
     g->stride = g->padl + rk::round64(g->W);
-    g->rows = rk::n_rows(c->L) + 1;
-    const int64_t elems = 2 * rk::table_rows(c->L) * (int64_t)g->stride;
+    g->rows = rk::n_rows(c->h.L) + 1;
+    const int64_t elems = 2 * rk::table_rows(c->h.L) * (int64_t)g->stride;
     if (elems <= 0 || elems > (int64_t(1) << 40)) return RK_E_NOMEM;
     // the products address each operand block with 32-bit byte offsets from its first row;
     // the widest block spans OFFSET_SPAN_L (L - 1) + OFFSET_SPAN_C rows
-    if ((rk::OFFSET_SPAN_L * (int64_t)c->L + rk::OFFSET_SPAN_C) * g->stride * 4 >= (int64_t(1) << 31))
+    if ((rk::OFFSET_SPAN_L * (int64_t)c->h.L + rk::OFFSET_SPAN_C) * g->stride * 4 >= (int64_t(1) << 31))
         return RK_E_NOMEM;
     *bytes = (size_t)elems * sizeof(int32_t);
     return RK_OK;
-}
-
-// Option slots of every block for the kernels: the kept options (every option when pruning
-// is off) in the caller's order, then padding up to the largest count.  A padding slot costs
-// the device infinity and needs only x_{s+1}: wherever it is a candidate its value is at or
-// above infinity, so it never changes a minimum and is never the recorded choice.
-void build_run(rk_chain *c)
-{
-    const int32_t L = c->L, K = c->K;
-    c->run_prune = c->prune;
-    int32_t kr = 1;
-    for (int32_t s = 0; s < L; ++s) {
-        int32_t n = 0;
-        for (int32_t o = 0; o < K; ++o) n += !c->prune || c->kept[(size_t)s * K + o];
-        kr = std::max(kr, n);
-    }
-    c->k_run = kr;
-    const size_t nr = (size_t)L * kr;
-    c->run_opt.assign(nr, -1);
-    c->run_xbar.assign(nr, 0);
-    c->run_c1.assign(nr, DINF);
-    c->run_need1.assign(nr, 0);
-    c->run_need1max.assign(L, 0);
-    for (int32_t s = 0; s < L; ++s) {
-        int32_t slot = 0;
-        for (int32_t o = 0; o < K; ++o) {
-            const size_t j = (size_t)s * K + o;
-            if (c->prune && !c->kept[j]) continue;
-            const size_t r = (size_t)s * kr + slot++;
-            c->run_opt[r] = o;
-            c->run_xbar[r] = c->xbar[j];
-            c->run_c1[r] = c->c1[j];
-            c->run_need1[r] = c->need1[j];
-            c->run_need1max[s] = std::max(c->run_need1max[s], c->need1[j]);
-        }
-        for (; slot < kr; ++slot) {
-            const size_t r = (size_t)s * kr + slot;
-            c->run_xbar[r] = c->run_need1[r] = c->x[s + 1];
-        }
-    }
 }
 
 // First solve on a device (or the first after the pruning switch changed): upload the
 // derived arrays; create the events and streams once.
 int ensure_device(rk_chain *c)
 {
-    if (c->d_chain && c->run_prune == c->prune) return RK_OK;
+    if (c->d_chain && c->run_prune == c->prune && c->run_version == c->host_version) return RK_OK;
     if (c->d_chain) {  // rebuild: the captured launch sequence holds the old arrays
         if (c->queued) HIPCHK(hipEventSynchronize(c->ev_fill1));
         HIPCHK(hipFree(c->d_chain));
@@ -167,8 +119,10 @@ int ensure_device(rk_chain *c)
         c->queued = false;
         c->bt_fill = -1;
     }
-    build_run(c);
-    const int32_t L = c->L, K = c->k_run;
+    rk::host_run_slots(c->h, c->prune, c->run);
+    c->run_prune = c->prune;
+    c->run_version = c->host_version;
+    const int32_t L = c->h.L, K = c->run.k_run;
     const size_t nx = L + 1, nk = (size_t)L * K, nl = (size_t)L * L, nr = (size_t)rk::n_rows(L);
     const size_t total = nx + 3 * nk + L + 2 * nl + nr;
     HIPCHK(hipMalloc(&c->d_chain, total * sizeof(int32_t)));
@@ -183,17 +137,17 @@ int ensure_device(rk_chain *c)
     };
     c->dc.L = L;
     c->dc.K = K;
-    c->dc.x = put(c->x);
-    c->dc.xbar = put(c->run_xbar);
-    c->dc.c1 = put(c->run_c1);
-    c->dc.need1 = put(c->run_need1);
-    c->dc.need1max = put(c->run_need1max);
-    c->dc.P = put(c->P);
-    c->dc.need2 = put(c->need2);
-    c->dc.lb = put(c->lb);
-    c->dc.h_msa = c->msa.data();
+    c->dc.x = put(c->h.x);
+    c->dc.xbar = put(c->run.xbar);
+    c->dc.c1 = put(c->run.c1);
+    c->dc.need1 = put(c->run.need1);
+    c->dc.need1max = put(c->run.need1max);
+    c->dc.P = put(c->h.P);
+    c->dc.need2 = put(c->h.need2);
+    c->dc.lb = put(c->h.lb);
+    c->dc.h_msa = c->h.msa.data();
     int64_t xbar_max = 0;
-    for (int32_t v : c->run_xbar) xbar_max = std::max<int64_t>(xbar_max, v);
+    for (int32_t v : c->run.xbar) xbar_max = std::max<int64_t>(xbar_max, v);
     c->dc.xbar_halo = xbar_max > rk::HMAX ? rk::HMAX + 1 : rk::round64(xbar_max);
     if (!c->dc.x || !c->dc.xbar || !c->dc.c1 || !c->dc.need1 || !c->dc.need1max || !c->dc.P ||
         !c->dc.need2 || !c->dc.lb) {  // leave no half-uploaded arrays behind: the next solve uploads again
@@ -255,7 +209,7 @@ int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t
     c->tb.stride = g.stride;
     c->tb.inf_row = g.rows - 1;
     c->tb.opt = tables + rk::SLACK * (int64_t)g.stride;
-    c->tb.ap = c->tb.opt + rk::table_rows(c->L) * (int64_t)g.stride;
+    c->tb.ap = c->tb.opt + rk::table_rows(c->h.L) * (int64_t)g.stride;
     c->stream = stream;
     HIPCHK(hipEventRecord(c->ev_fill0, stream));
     const bool replay = c->gexec && c->g_M == M && c->g_tables == tables && c->g_stream == stream &&
@@ -309,9 +263,9 @@ int answer(rk_chain *c, int32_t *out)
 {
     if (!c->queued) return RK_E_NOT_SOLVED;
     HIPCHK(hipEventSynchronize(c->ev_fill1));
-    if (c->M < c->x[0]) { *out = RK_INF; return RK_OK; }
+    if (c->M < c->h.x[0]) { *out = RK_INF; return RK_OK; }
     int32_t v = 0;
-    const int64_t idx = rk::row_of(c->L, 0, c->L - 1) * c->tb.stride + c->tb.padl + (c->M - c->x[0]);
+    const int64_t idx = rk::row_of(c->h.L, 0, c->h.L - 1) * c->tb.stride + c->tb.padl + (c->M - c->h.x[0]);
     HIPCHK(hipMemcpy(&v, c->tb.opt + idx, sizeof(int32_t), hipMemcpyDeviceToHost));
     *out = to_abi(v);
     return RK_OK;
@@ -328,114 +282,18 @@ int rk_chain_create(int32_t L, int32_t K, const int32_t *x, const int32_t *fn_ti
 {
     if (!out) return RK_E_INVAL;
     *out = nullptr;
-    if (L < 1 || L > RK_MAX_L || K < 1 || (int64_t)L + K >= 32768) return RK_E_INVAL;
-    if (!x || !fn_time || !fn_tmp || !fwd || !bwd || !mem || !tmp_fwd || !tmp_bwd) return RK_E_INVAL;
-    const int64_t nk = (int64_t)L * K;
-    for (int32_t i = 0; i <= L; ++i)
-        if (x[i] < 0) return RK_E_INVAL;
-    for (int32_t i = 0; i < L; ++i)
-        if (fn_time[i] < 0 || fn_tmp[i] < 0) return RK_E_INVAL;
-    for (int64_t j = 0; j < nk; ++j)
-        if (fwd[j] < 0 || bwd[j] < 0 || mem[j] < 0 || tmp_fwd[j] < 0 || tmp_bwd[j] < 0)
-            return RK_E_INVAL;
-    // Bound on any schedule's time: a block is forwarded at most L times, backwarded once.
-    int64_t fsum = 0, bsum = 0;
-    for (int32_t i = 0; i < L; ++i) {
-        int64_t fm = fn_time[i], bm = 0;
-        for (int32_t o = 0; o < K; ++o) {
-            fm = std::max<int64_t>(fm, fwd[(int64_t)i * K + o]);
-            bm = std::max<int64_t>(bm, bwd[(int64_t)i * K + o]);
-        }
-        fsum += fm;
-        bsum += bm;
-    }
-    if ((int64_t)L * fsum + bsum > RK_TIME_LIMIT) return RK_E_OVERFLOW;
-
     rk_chain *c = new (std::nothrow) rk_chain;
     if (!c) return RK_E_NOMEM;
+    int rc;
     try {
-        c->L = L;
-        c->K = K;
-        c->x.assign(x, x + L + 1);
-        c->xbar.resize(nk);
-        c->c1.resize(nk);
-        c->need1.resize(nk);
-        c->kept.assign(nk, 1);
-        c->P.assign((size_t)L * L, 0);
-        c->need2.assign((size_t)L * L, 0);
-        c->msa.assign((size_t)rk::n_rows(L), 0);
-        c->lb.assign((size_t)rk::n_rows(L), 0);
+        rc = rk::host_create(c->h, L, K, x, fn_time, fn_tmp, fwd, bwd, mem, tmp_fwd, tmp_bwd);
     } catch (...) {
+        rc = RK_E_NOMEM;
+    }
+    if (rc != RK_OK) {
         delete c;
-        return RK_E_NOMEM;
+        return rc;
     }
-    // Case 1 (Eq. fe): F_s^o leaves xbar = x_{s+1} + mem live; it and B_s^o need their
-    // temporary memory on top of that; the pair costs r(F_s^o) + r(B_s^o).
-    for (int32_t s = 0; s < L; ++s)
-        for (int32_t o = 0; o < K; ++o) {
-            const int64_t j = (int64_t)s * K + o;
-            const int64_t xb = (int64_t)x[s + 1] + mem[j];
-            c->xbar[j] = (int32_t)std::min(xb, kSizeCap);
-            c->need1[j] = (int32_t)std::min(xb + std::max(tmp_fwd[j], tmp_bwd[j]), kSizeCap);
-            c->c1[j] = fwd[j] + bwd[j];
-        }
-    // Option o of block s is never the recorded choice when an earlier option o' < o of the
-    // block is at least as good in all that Eq. fe reads: r(F)+r(B), xbar and the memory the
-    // pair needs.  Then o' is a candidate wherever o is, and (Opt being non-increasing in m)
-    // never costs more; at equal cost it wins by its smaller code.  Testing against the kept
-    // options suffices: dominance is transitive.  This also drops repeated options, which the
-    // paper's budget grid produces many of (Sec. 3, Phase 2).
-    for (int32_t s = 0; s < L; ++s)
-        for (int32_t o = 1; o < K; ++o) {
-            const int64_t j = (int64_t)s * K + o;
-            for (int32_t q = 0; q < o; ++q) {
-                const int64_t i = (int64_t)s * K + q;
-                if (c->kept[i] && c->c1[i] <= c->c1[j] && c->xbar[i] <= c->xbar[j] && c->need1[i] <= c->need1[j]) {
-                    c->kept[j] = 0;
-                    break;
-                }
-            }
-        }
-    // Case 2 (Eq. fn): the sweep F_s^0..F_{i-1}^0 costs P[s][i]; F_k^0 holds its input
-    // (except the span input x_s, outside the budget), its output and tmp(F_k^0).
-    for (int32_t s = 0; s < L; ++s) {
-        int64_t p = 0, need = 0;
-        for (int32_t i = s + 1; i < L; ++i) {
-            const int32_t k = i - 1;
-            p += fn_time[k];
-            need = std::max<int64_t>(need, (k > s ? (int64_t)x[k] : 0) + x[k + 1] + fn_tmp[k]);
-            c->P[(size_t)s * L + i] = (int32_t)p;
-            c->need2[(size_t)s * L + i] = (int32_t)std::min(need, kSizeCap);
-        }
-    }
-    // Storing everything: every schedule of a span runs each of its blocks' backward once,
-    // paired with one saving forward, so it costs at least lb(s,t) = sum of min_o r(F)+r(B)
-    // (further forwards only add).  Case 1 with a cheapest option at every block reaches lb
-    // as soon as it fits, from msa(s,t) = min over the cheapest options o of block s of
-    // max(need1[s][o], xbar[s][o] + msa(s+1,t)) (msa(s,s): the smallest need1).  Opt being
-    // non-increasing in m, Opt(s,t,m) = lb(s,t) for every m >= msa(s,t).
-    {
-        std::vector<int64_t> cmin(L), prefix(L + 1, 0);
-        for (int32_t s = 0; s < L; ++s) {
-            int64_t v = INT64_MAX;
-            for (int32_t o = 0; o < K; ++o) v = std::min<int64_t>(v, c->c1[(size_t)s * K + o]);
-            cmin[s] = v;
-            prefix[s + 1] = prefix[s] + v;
-        }
-        for (int32_t t = 0; t < L; ++t)
-            for (int32_t s = t; s >= 0; --s) {
-                const int64_t rest = s < t ? c->msa[(size_t)rk::row_of(L, s + 1, t)] : 0;
-                int64_t best = kSizeCap;
-                for (int32_t o = 0; o < K; ++o) {
-                    const size_t j = (size_t)s * K + o;
-                    if (c->c1[j] != cmin[s]) continue;
-                    best = std::min(best, std::max<int64_t>(c->need1[j], s < t ? c->xbar[j] + rest : 0));
-                }
-                c->msa[(size_t)rk::row_of(L, s, t)] = (int32_t)std::min(best, kSizeCap);
-                c->lb[(size_t)rk::row_of(L, s, t)] = (int32_t)(prefix[t + 1] - prefix[s]);
-            }
-    }
-    for (int32_t i = 1; i < L; ++i) c->max_x = std::max(c->max_x, x[i]);
     *out = c;
     return RK_OK;
 }
@@ -558,7 +416,7 @@ int rk_extract_schedule(rk_chain *c, rk_op *ops, int64_t cap, int64_t *n_ops, in
     if (rc != RK_OK) return rc;
     if (ans == RK_INF) return RK_E_INFEASIBLE;
     // At most L forwards per block (one saving) and one backward, one forget per no-save forward.
-    const int64_t max_ops = 2 * (int64_t)c->L * c->L + 16;
+    const int64_t max_ops = 2 * (int64_t)c->h.L * c->h.L + 16;
     if (c->d_ops_cap < max_ops) {
         if (c->d_ops) HIPCHK(hipFree(c->d_ops));
         c->d_ops = nullptr;
@@ -571,7 +429,7 @@ int rk_extract_schedule(rk_chain *c, rk_op *ops, int64_t cap, int64_t *n_ops, in
     int64_t *const res = c->bt_res;
     if (c->bt_fill != c->fills) {
         c->bt_fill = -1;
-        HIPCHK(rk::launch_backtrace(c->dc, c->tb, c->M - c->x[0], c->d_ops, c->d_ops_cap, c->d_res,
+        HIPCHK(rk::launch_backtrace(c->dc, c->tb, c->M - c->h.x[0], c->d_ops, c->d_ops_cap, c->d_res,
                                     c->stream));
         HIPCHK(hipMemcpyAsync(res, c->d_res, 3 * sizeof(int64_t), hipMemcpyDeviceToHost, c->stream));
         HIPCHK(hipStreamSynchronize(c->stream));
@@ -584,18 +442,18 @@ int rk_extract_schedule(rk_chain *c, rk_op *ops, int64_t cap, int64_t *n_ops, in
     HIPCHK(hipMemcpy(ops, c->d_ops, res[0] * sizeof(rk_op), hipMemcpyDeviceToHost));
     for (int64_t k = 0; k < res[0]; ++k)  // option slots back to the caller's option indices
         if (ops[k].kind == RK_FWD_SAVE || ops[k].kind == RK_BWD)
-            ops[k].option = c->run_opt[(size_t)ops[k].block * c->k_run + ops[k].option];
+            ops[k].option = c->run.opt[(size_t)ops[k].block * c->run.k_run + ops[k].option];
     return RK_OK;
 }
 
 int rk_read_row(rk_chain *c, int32_t s, int32_t t, int32_t *opt_row, int16_t *arg_row)
 {
-    if (!c || s < 0 || t < s || t >= c->L) return RK_E_INVAL;
+    if (!c || s < 0 || t < s || t >= c->h.L) return RK_E_INVAL;
     if (!c->queued) return RK_E_NOT_SOLVED;
     DeviceScope ds(c);
     if (!ds.ok) return RK_E_DEVICE;
     HIPCHK(hipEventSynchronize(c->ev_fill1));
-    const int64_t base = rk::row_of(c->L, s, t) * c->tb.stride + c->tb.padl;
+    const int64_t base = rk::row_of(c->h.L, s, t) * c->tb.stride + c->tb.padl;
     if (opt_row) {
         HIPCHK(hipMemcpy(opt_row, c->tb.opt + base, (size_t)c->W * sizeof(int32_t), hipMemcpyDeviceToHost));
         for (int32_t m = 0; m < c->W; ++m) opt_row[m] = to_abi(opt_row[m]);
@@ -613,7 +471,7 @@ int rk_read_row(rk_chain *c, int32_t s, int32_t t, int32_t *opt_row, int16_t *ar
                               hipMemcpyDeviceToHost, c->stream));
         HIPCHK(hipStreamSynchronize(c->stream));
         for (int32_t m = 0; m < c->W; ++m)  // option slots back to the caller's option indices
-            if (arg_row[m] >= c->L) arg_row[m] = (int16_t)(c->L + c->run_opt[(size_t)s * c->k_run + (arg_row[m] - c->L)]);
+            if (arg_row[m] >= c->h.L) arg_row[m] = (int16_t)(c->h.L + c->run.opt[(size_t)s * c->run.k_run + (arg_row[m] - c->h.L)]);
     }
     return RK_OK;
 }
@@ -627,10 +485,10 @@ int rk_tradeoff_curve(rk_chain *c, int32_t *times, int64_t n)
     if (!ds.ok) return RK_E_DEVICE;
     HIPCHK(hipEventSynchronize(c->ev_fill1));
     // budget b leaves b - x_0 slots beyond the chain input: Opt(0, L-1, b - x_0)
-    const int64_t x0 = c->x[0], lead = std::min<int64_t>(n, x0);
+    const int64_t x0 = c->h.x[0], lead = std::min<int64_t>(n, x0);
     for (int64_t b = 0; b < lead; ++b) times[b] = RK_INF;
     if (n > x0) {
-        const int64_t base = rk::row_of(c->L, 0, c->L - 1) * c->tb.stride + c->tb.padl;
+        const int64_t base = rk::row_of(c->h.L, 0, c->h.L - 1) * c->tb.stride + c->tb.padl;
         HIPCHK(hipMemcpy(times + x0, c->tb.opt + base, (size_t)(n - x0) * sizeof(int32_t), hipMemcpyDeviceToHost));
         for (int64_t b = x0; b < n; ++b) times[b] = to_abi(times[b]);
     }
@@ -696,11 +554,11 @@ int rk_chain_options(const rk_chain *c, int32_t *kept, int32_t *k_run)
 {
     if (!c) return RK_E_INVAL;
     int32_t kr = 1;
-    for (int32_t s = 0; s < c->L; ++s) {
+    for (int32_t s = 0; s < c->h.L; ++s) {
         int32_t n = 0;
-        for (int32_t o = 0; o < c->K; ++o) {
-            const size_t j = (size_t)s * c->K + o;
-            const int32_t v = !c->prune || c->kept[j];
+        for (int32_t o = 0; o < c->h.K; ++o) {
+            const size_t j = (size_t)s * c->h.K + o;
+            const int32_t v = !c->prune || c->h.kept[j];
             if (kept) kept[j] = v;
             n += v;
         }
