@@ -7,10 +7,12 @@ from paper_2307_01236_amd import calib
 pytestmark = pytest.mark.gpu
 
 
-def test_valu_rate_below_nominal_peak():
+def test_valu_rate_near_nominal_peak():
+    """k_valu runs exactly 2 VALU instructions per step (SQ_INSTS_VALU per wave =
+    16 x iterations + 17, profiles/valu_ceiling_k_valu.md), so its rate cannot pass the
+    nominal peak by more than the clock allows: runs measure 97-105% of 39.32 T."""
     r = calib.valu_int32_rate(1 << 12)
-    # runs have measured up to 5% above the nominal figure (clock above 2.4 GHz)
-    assert 0.3 * 39.3e12 < r < 1.15 * 39.3e12, r
+    assert 0.5 * 39.32e12 < r < 1.08 * 39.32e12, r
 
 
 def test_copy_bandwidth_below_hbm_peak():
