@@ -49,7 +49,7 @@ extern "C" {
 #define RK_MAX_L 2000                     /* longest chain                                */
 #define RK_MAX_M ((int32_t)((1 << 26) - 2))       /* largest budget                       */
 
-enum { RK_FWD_NOSAVE = 0, RK_FWD_SAVE = 1, RK_BWD = 2, RK_FREE_X = 3 };
+enum { RK_FWD_NOSAVE = 0, RK_FWD_SAVE = 1, RK_BWD = 2, RK_FREE_X = 3, RK_REFWD = 4 };
 
 enum {
     RK_OK = 0,
@@ -64,8 +64,9 @@ enum {
 };
 
 /* One schedule step.  kind: RK_FWD_NOSAVE (F_block^0), RK_FWD_SAVE (F_block^option),
- * RK_BWD (B_block^option), RK_FREE_X (drop activation x_block).  option is -1 for
- * RK_FWD_NOSAVE and RK_FREE_X. */
+ * RK_BWD (B_block^option), RK_FREE_X (drop activation x_block), RK_REFWD (make
+ * x_{block+1} again from the intermediates F_block^option kept; the saving sweep only).
+ * option is -1 for RK_FWD_NOSAVE and RK_FREE_X. */
 typedef struct { int32_t kind, block, option; } rk_op;
 
 typedef struct rk_chain rk_chain;
@@ -84,6 +85,28 @@ int rk_chain_create(int32_t L, int32_t K, const int32_t *x, const int32_t *fn_ti
                     const int32_t *fn_tmp, const int32_t *fwd, const int32_t *bwd,
                     const int32_t *mem, const int32_t *tmp_fwd, const int32_t *tmp_bwd,
                     rk_chain **out);
+
+/*
+ * The saving sweep: this library's reading of the sub-optimality remark (ii) of Sec. 3.4
+ * (a forward that runs several times may keep intermediate data on its first pass and use
+ * it to make its output faster on later passes).  It adds a third case to Eq. all for a
+ * span (s,t) with t >= s+2 and a saving option o of block s: F_s^o keeps its intermediates,
+ * the no-save forwards F_{s+1}^0 .. F_{i-1}^0 run to x_i dropping everything behind them
+ * (x_{s+1} included), blocks i..t are solved with x_i held, x_i is dropped, x_{s+1} is made
+ * again from the kept data (an RK_REFWD step of time refwd[s*K+o] and temporary memory
+ * tmp_fwd[s*K+o]), blocks s+1..i-1 are solved, and B_s^o ends the span:
+ *   Opt_3(s,t,m) = min_o r(F_s^o) + r(B_s^o) + refwd_s^o + H(s+1, t, m - mem_s^o),
+ *   H(s',t,u)   = min_{i=s'+1..t} sum_{k=s'}^{i-1} r(F_k^0) + Opt(i,t,u - x_i) + Opt(s',i-1,u - x_s'),
+ * valid where case 1 with o is, and where every F_k^0 of the sweep fits u with its input,
+ * its output and tmp(F_k^0).  The recorded choice of case 3 has code L + K + o (after case
+ * 2's codes i and case 1's codes L + o).
+ * refwd: host [L*K] re-forward times (deep-copied), or NULL to switch the case off (the
+ * default).  Takes effect at the next solve; the workspace of a solve with the case on
+ * holds twice the tables.  RK_E_INVAL for a negative time or L + 2K >= 32768,
+ * RK_E_OVERFLOW when L * sum_i max(r(F_i^0), max_o r(F_i^o), max_o refwd_i^o) +
+ * sum_i max_o r(B_i^o) exceeds RK_TIME_LIMIT; the chain is unchanged then.
+ */
+int rk_chain_set_saving_sweep(rk_chain *c, const int32_t *refwd);
 
 /* Release the chain, its device copies and any table it allocated.  NULL is a no-op. */
 void rk_chain_destroy(rk_chain *c);

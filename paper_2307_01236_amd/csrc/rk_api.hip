@@ -95,7 +95,8 @@ int geometry(const rk_chain *c, int32_t M, Geometry *g, size_t *bytes)
     g->padl = rk::round64(std::min<int64_t>(c->h.max_x, g->W));
     g->stride = g->padl + rk::round64(g->W);
     g->rows = rk::n_rows(c->h.L) + 1;
-    const int64_t elems = 2 * rk::table_rows(c->h.L) * (int64_t)g->stride;
+    // Opt and ap; with the saving sweep also H and aq
+    const int64_t elems = (c->h.refwd.empty() ? 2 : 4) * rk::table_rows(c->h.L) * (int64_t)g->stride;
     if (elems <= 0 || elems > (int64_t(1) << 40)) return RK_E_NOMEM;
     // the products address each operand block with 32-bit byte offsets from its first row;
     // the widest block spans OFFSET_SPAN_L (L - 1) + OFFSET_SPAN_C rows
@@ -123,8 +124,9 @@ int ensure_device(rk_chain *c)
     c->run_prune = c->prune;
     c->run_version = c->host_version;
     const int32_t L = c->h.L, K = c->run.k_run;
+    const bool sweep = !c->h.refwd.empty();
     const size_t nx = L + 1, nk = (size_t)L * K, nl = (size_t)L * L, nr = (size_t)rk::n_rows(L);
-    const size_t total = nx + 3 * nk + L + 2 * nl + nr;
+    const size_t total = nx + 3 * nk + L + 2 * nl + nr + (sweep ? nk + nl : 0);
     HIPCHK(hipMalloc(&c->d_chain, total * sizeof(int32_t)));
     int32_t *p = static_cast<int32_t *>(c->d_chain);
     size_t off = 0;
@@ -145,12 +147,14 @@ int ensure_device(rk_chain *c)
     c->dc.P = put(c->h.P);
     c->dc.need2 = put(c->h.need2);
     c->dc.lb = put(c->h.lb);
+    c->dc.c3 = sweep ? put(c->run.c3) : nullptr;
+    c->dc.need3 = sweep ? put(c->h.need3) : nullptr;
     c->dc.h_msa = c->h.msa.data();
     int64_t xbar_max = 0;
     for (int32_t v : c->run.xbar) xbar_max = std::max<int64_t>(xbar_max, v);
     c->dc.xbar_halo = xbar_max > rk::HMAX ? rk::HMAX + 1 : rk::round64(xbar_max);
     if (!c->dc.x || !c->dc.xbar || !c->dc.c1 || !c->dc.need1 || !c->dc.need1max || !c->dc.P ||
-        !c->dc.need2 || !c->dc.lb) {  // leave no half-uploaded arrays behind: the next solve uploads again
+        !c->dc.need2 || !c->dc.lb || (sweep && (!c->dc.c3 || !c->dc.need3))) {  // leave no half-uploaded arrays behind: the next solve uploads again
         (void)hipFree(c->d_chain);
         c->d_chain = nullptr;
         return RK_E_DEVICE;
@@ -208,8 +212,11 @@ int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t
     c->tb.padl = g.padl;
     c->tb.stride = g.stride;
     c->tb.inf_row = g.rows - 1;
+    const int64_t tsz = rk::table_rows(c->h.L) * (int64_t)g.stride;
     c->tb.opt = tables + rk::SLACK * (int64_t)g.stride;
-    c->tb.ap = c->tb.opt + rk::table_rows(c->h.L) * (int64_t)g.stride;
+    c->tb.ap = c->tb.opt + tsz;
+    c->tb.hopt = c->dc.c3 ? c->tb.ap + tsz : nullptr;
+    c->tb.aq = c->dc.c3 ? c->tb.ap + 2 * tsz : nullptr;
     c->stream = stream;
     HIPCHK(hipEventRecord(c->ev_fill0, stream));
     const bool replay = c->gexec && c->g_M == M && c->g_tables == tables && c->g_stream == stream &&
@@ -298,6 +305,21 @@ int rk_chain_create(int32_t L, int32_t K, const int32_t *x, const int32_t *fn_ti
     return RK_OK;
 }
 
+int rk_chain_set_saving_sweep(rk_chain *c, const int32_t *refwd)
+{
+    if (!c) return RK_E_INVAL;
+    int rc;
+    try {
+        rk::HostChain h = c->h;  // left unchanged on an error
+        rc = rk::host_set_refwd(h, refwd);
+        if (rc == RK_OK) c->h.refwd.swap(h.refwd), c->h.c3.swap(h.c3), c->h.need3.swap(h.need3), c->h.kept.swap(h.kept);
+    } catch (...) {
+        rc = RK_E_NOMEM;
+    }
+    if (rc == RK_OK) ++c->host_version;  // the next solve rebuilds the device arrays
+    return rc;
+}
+
 void rk_chain_destroy(rk_chain *c)
 {
     if (!c) return;
@@ -339,7 +361,9 @@ int rk_solve_async(rk_chain *c, int32_t M, void *d_workspace, size_t ws_bytes, v
     hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
     if (stream && hipStreamIsCapturing(static_cast<hipStream_t>(stream), &cs) != hipSuccess) return RK_E_DEVICE;
     if (cs != hipStreamCaptureStatusNone) {
-        if (!c->d_chain || c->run_prune != c->prune || !d_workspace || c->prof.on) return RK_E_INVAL;
+        if (!c->d_chain || c->run_prune != c->prune || c->run_version != c->host_version || !d_workspace ||
+            c->prof.on)
+            return RK_E_INVAL;
         if (ws_bytes < need) return RK_E_NOMEM;
         return fill(c, M, g, static_cast<int32_t *>(d_workspace), static_cast<hipStream_t>(stream), true);
     }
@@ -375,7 +399,8 @@ int rk_solve_noalloc(rk_chain *c, int32_t M, void *stream)
     if (rc != RK_OK) return rc;
     if (need > RK_NOALLOC_MAX_BYTES) return RK_E_NOMEM;
     // the derived arrays, events and stream exist from an earlier solve on this device
-    if (!c->d_chain || c->run_prune != c->prune || c->prof.on || !c->ev_fill0 || !c->ev_fill1)
+    if (!c->d_chain || c->run_prune != c->prune || c->run_version != c->host_version || c->prof.on ||
+        !c->ev_fill0 || !c->ev_fill1)
         return RK_E_INVAL;
     DeviceScope ds(c);
     if (!ds.ok) return RK_E_DEVICE;
@@ -416,7 +441,9 @@ int rk_extract_schedule(rk_chain *c, rk_op *ops, int64_t cap, int64_t *n_ops, in
     if (rc != RK_OK) return rc;
     if (ans == RK_INF) return RK_E_INFEASIBLE;
     // At most L forwards per block (one saving) and one backward, one forget per no-save forward.
-    const int64_t max_ops = 2 * (int64_t)c->h.L * c->h.L + 16;
+    // At most L forwards per block (one saving, one re-forward with the saving sweep) and one
+    // backward, one forget per no-save forward.
+    const int64_t max_ops = 3 * (int64_t)c->h.L * c->h.L + 16;
     if (c->d_ops_cap < max_ops) {
         if (c->d_ops) HIPCHK(hipFree(c->d_ops));
         c->d_ops = nullptr;
@@ -441,7 +468,7 @@ int rk_extract_schedule(rk_chain *c, rk_op *ops, int64_t cap, int64_t *n_ops, in
     if (!ops || cap < res[0]) return RK_E_BUFSZ;
     HIPCHK(hipMemcpy(ops, c->d_ops, res[0] * sizeof(rk_op), hipMemcpyDeviceToHost));
     for (int64_t k = 0; k < res[0]; ++k)  // option slots back to the caller's option indices
-        if (ops[k].kind == RK_FWD_SAVE || ops[k].kind == RK_BWD)
+        if (ops[k].kind == RK_FWD_SAVE || ops[k].kind == RK_BWD || ops[k].kind == RK_REFWD)
             ops[k].option = c->run.opt[(size_t)ops[k].block * c->run.k_run + ops[k].option];
     return RK_OK;
 }
@@ -471,7 +498,11 @@ int rk_read_row(rk_chain *c, int32_t s, int32_t t, int32_t *opt_row, int16_t *ar
                               hipMemcpyDeviceToHost, c->stream));
         HIPCHK(hipStreamSynchronize(c->stream));
         for (int32_t m = 0; m < c->W; ++m)  // option slots back to the caller's option indices
-            if (arg_row[m] >= c->h.L) arg_row[m] = (int16_t)(c->h.L + c->run.opt[(size_t)s * c->run.k_run + (arg_row[m] - c->h.L)]);
+            if (arg_row[m] >= c->h.L + c->run.k_run)  // case 3 (the saving sweep)
+                arg_row[m] = (int16_t)(c->h.L + c->h.K +
+                                       c->run.opt[(size_t)s * c->run.k_run + (arg_row[m] - c->h.L - c->run.k_run)]);
+            else if (arg_row[m] >= c->h.L)
+                arg_row[m] = (int16_t)(c->h.L + c->run.opt[(size_t)s * c->run.k_run + (arg_row[m] - c->h.L)]);
     }
     return RK_OK;
 }

@@ -18,6 +18,7 @@
 //   ap   the left operand of Eq. fn, precomputed when a row becomes final:
 //        ap[row(s,i-1)*stride + padl + m] = P[s][i] + Opt(s,i-1,m) if the
 //        no-save sweep s..i-1 fits in m, else infinity (saturated).
+//   hopt, aq  (the saving sweep only) H of case 3 and its left operand, laid out alike.
 //
 // Inside the device code "infinity" is DINF = 2^30 - 1: ap (at most DINF) plus
 // an Opt value (at most DINF) fits in int32, so the hot loops are a plain add
@@ -80,6 +81,10 @@ struct DevChain {
     // uses it to size each launch.
     const int32_t *lb;     // [L(L+1)/2]
     const int32_t *h_msa;  // [L(L+1)/2], host memory
+    // The saving sweep (both null when it is off): c3 = r(F)+r(B)+refwd per option slot
+    // [L*K], need3 [L*L] the thresholds of the sweeps of H (the input inside the budget).
+    const int32_t *c3;
+    const int32_t *need3;
     int32_t xbar_halo;     // round64(max xbar): how far left case 1 reads from column m
 };
 
@@ -89,6 +94,11 @@ constexpr int32_t HMAX = 256;
 struct Tables {
     int32_t *opt;
     int32_t *ap;
+    // with the saving sweep (else null): H(s,t,u) and its left operand
+    // aq[row(s,i-1)*stride + padl + v] = P[s][i] + Opt(s,i-1,v) if the sweep s..i-1 with its
+    // input fits v + x_s, else infinity (H reads it at v = u - x_s)
+    int32_t *hopt;
+    int32_t *aq;
     int32_t W, stride, padl;
     int64_t inf_row;  // index of the all-infinity row (= number of span rows)
 };

@@ -57,17 +57,17 @@ static hipError_t launch(Profiler *prof, int32_t kind, K kernel, dim3 grid, dim3
 }
 
 // ---------------------------------------------------------------------------------------
-// The all-infinity row and the slack rows of both tables (read in place of operands that
+// The all-infinity row and the slack rows of every table (read in place of operands that
 // do not exist yet).  Block y picks the row: slack before row 0, or the infinity row and
-// the slack after it, of either table.
+// the slack after it, of table y / (2 SLACK + 1) (opt, ap, then hopt and aq).
 // ---------------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_init_inf_rows(Tables tb)
 {
     constexpr int32_t PER_TABLE = 2 * SLACK + 1;
     const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const int32_t y = (int32_t)blockIdx.y, k = y % PER_TABLE;
+    const int32_t y = (int32_t)blockIdx.y, k = y % PER_TABLE, table = y / PER_TABLE;
     const int64_t row = k < SLACK ? (int64_t)k - SLACK : tb.inf_row + (k - SLACK);
-    int32_t *const base = y < PER_TABLE ? tb.opt : tb.ap;
+    int32_t *const base = table == 0 ? tb.opt : table == 1 ? tb.ap : table == 2 ? tb.hopt : tb.aq;
     if (j < tb.stride) base[row * tb.stride + j] = DINF;
 }
 
@@ -144,7 +144,8 @@ __device__ inline uint32_t buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uin
 }
 
 template <int SR, int TW, int TH, int NW>
-__global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int32_t tau, int32_t n_chunks)
+__global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int32_t tau, int32_t n_chunks,
+                                                     int32_t n_chunks_h)
 {
     // TH waves share SR rows, each keeping TW of the T = TW TH ends of those rows
     constexpr int T = TW * TH, SW = SR * NW / TH, CI = PROD_CI;
@@ -166,7 +167,14 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
     const uint32_t n_rb = (uint32_t)(s_end + SW - 1) / SW;
     int32_t chunk, rb;  // row blocks of a column chunk adjacent, chunks spread over the XCDs
     chunk_tile(blockIdx.x, n_rb, &chunk, &rb);
-    if (chunk >= n_chunks) return;
+    if (chunk >= n_chunks + n_chunks_h) return;
+    // The first n_chunks chunks: case 2 of Opt (left operand ap, partials into opt).  With
+    // the saving sweep, n_chunks_h more: H (left operand aq read x_s columns to the left,
+    // partials into hopt).  The right operand is Opt in both.
+    const bool hp = chunk >= n_chunks;
+    if (hp) chunk -= n_chunks;
+    const int32_t *const left = hp ? tb.aq : tb.ap;
+    int32_t *const out = hp ? tb.hopt : tb.opt;
     const int32_t S0 = rb * SW;
     const uint32_t mchunk = (uint32_t)chunk;
     const int32_t rg = wave / TH, kh = (wave % TH) * TW;  // row group, first end offset
@@ -177,7 +185,7 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
     const uint32_t colb = (uint32_t)(padl + min(m, (uint32_t)tb.W - 1)) * 4u;
     const uint32_t pitch = (uint32_t)stride * 4u;
     const int32_t *const opt_end = tb.opt + (tb.inf_row + 1 + SLACK) * stride;
-    const int32_t *const ap_end = tb.ap + (tb.inf_row + 1 + SLACK) * stride;
+    const int32_t *const ap_end = left + (tb.inf_row + 1 + SLACK) * stride;
     const int32_t t0 = S0 + tau;  // first end the workgroup covers
     const int32_t i_lo = S0 + 1, i_hi = min(S0 + SW - 1 + tau, L - 1);
 
@@ -193,7 +201,8 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
         uint32_t delta = 0;
 #pragma unroll
         for (int r = 0; r < SR; ++r) {
-            aoff[r] = delta * pitch + colb;
+            // H reads aq(s, i, m - x_s); x_s <= padl unless padl >= W (the read then lands in the pad)
+            aoff[r] = delta * pitch + colb - (hp ? 4u * (uint32_t)min(ch.x[min(s0 + r, L)], padl) : 0u);
             delta += (uint32_t)(L - 1 - (s0 + r));
         }
     }
@@ -213,7 +222,7 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
     const int32_t *qcur = nullptr, *acur = nullptr;
     auto seek = [&](int32_t ic) {
         qcur = tb.opt + (row_of(L, ic, t0) - 1) * stride;
-        acur = tb.ap + row_of(L, s0, ic - 1) * stride;
+        acur = left + row_of(L, s0, ic - 1) * stride;
     };
     auto fetch = [&](int32_t ic) {
         // right operands from one row before (ic, t0): split i's rows start rel(i) rows on,
@@ -343,7 +352,7 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
 #pragma unroll
         for (int k = 0; k < TW; ++k) {
             const int32_t s = s0 + r, t = s + tau + kh + k;
-            if (s < s_end && t < L) tb.opt[row_of(L, s, t) * stride + padl + m] = (int32_t)acc[r][k];
+            if (s < s_end && t < L) out[row_of(L, s, t) * stride + padl + m] = (int32_t)acc[r][k];
         }
 }
 
@@ -382,7 +391,7 @@ constexpr int mid_rows() { return 4; }
 
 template <int WD, bool GA, bool LO0>
 __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t tau, int32_t accumulate,
-                                int32_t g)
+                                int32_t g, bool hp)
 {
     constexpr int R = mid_rows<WD>(), NS = WD + R - 1, NJ = R + WD - 1;
     static_assert(WD == 4 || WD == 8 || WD == 16, "widths 4, 8 and 16");
@@ -398,7 +407,12 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
     const int32_t m = mc * 64 + lane;
     const uint32_t col = (uint32_t)(padl + min(m, W - 1)) * 4u;
     const int32_t *const opt_end = tb.opt + (tb.inf_row + 1 + SLACK) * stride;
-    const int32_t *const ap_end = tb.ap + (tb.inf_row + 1 + SLACK) * stride;
+    // case 2 of Opt (left ap, into opt) or, with hp, H of the saving sweep (left aq read x_s
+    // columns to the left, into hopt)
+    const int32_t *const left = hp ? tb.aq : tb.ap;
+    int32_t *const out = hp ? tb.hopt : tb.opt;
+    const int32_t *const ap_end = left + (tb.inf_row + 1 + SLACK) * stride;
+    auto lsh = [&](int32_t srow) { return hp ? 4u * (uint32_t)min(ch.x[min(srow, L)], padl) : 0u; };
     auto rows_between = [&](int32_t s_from, int32_t s_to) {  // row(s_to, t) - row(s_from, t)
         return (int64_t)(s_to - s_from) * (L - 1) - ((int64_t)s_to * (s_to - 1) - (int64_t)s_from * (s_from - 1)) / 2;
     };
@@ -420,11 +434,13 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
 #pragma unroll
         for (int j = 0; j < NJ; ++j) xoff[j] = (uint32_t)j * pitch + col;
 #pragma unroll
-        for (int r = 0; r < R; ++r) roff[r] = (uint32_t)rows_between(base, min(base + r, L - 1)) * pitch + col;
+        for (int r = 0; r < R; ++r)
+            roff[r] = (uint32_t)rows_between(base, min(base + r, L - 1)) * pitch + col - lsh(base + r);
     } else {
         const int32_t sb = base - WD + 1;
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) xoff[j] = (uint32_t)rows_between(sa, max(sb + j, 0)) * pitch + col;
+        for (int j = 0; j < NJ; ++j)
+            xoff[j] = (uint32_t)rows_between(sa, max(sb + j, 0)) * pitch + col - lsh(max(sb + j, 0));
 #pragma unroll
         for (int r = 0; r < R; ++r) roff[r] = (uint32_t)r * pitch + col;
     }
@@ -445,7 +461,7 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
         const int32_t i = min(i0 + u, L - 1);
         const int32_t xs = xsh[u];
         const __amdgpu_buffer_rsrc_t dq = block_rsrc(tb.opt + row_of(L, i, base + tau) * stride - xs, opt_end);
-        const __amdgpu_buffer_rsrc_t da = block_rsrc(tb.ap + row_of(L, sa, i0 + u - 1) * stride, ap_end);
+        const __amdgpu_buffer_rsrc_t da = block_rsrc(left + row_of(L, sa, i0 + u - 1) * stride, ap_end);
 #pragma unroll
         for (int r = rlo; r <= rhi; ++r) vr[b][r] = buf_load(GA ? da : dq, roff[r], 0);
 #pragma unroll
@@ -519,7 +535,7 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
         const int32_t sr = base + r;  // group A: the row; group B: the row of span tau at end t0 + r
         const int32_t tr = base + r + tau;
         if (sr < L - tau) {  // some cell of this row (A) or end (B) lies in the table
-            int32_t *const rb = tb.opt + row_of(L, sr, tr) * stride;
+            int32_t *const rb = out + row_of(L, sr, tr) * stride;
             int64_t back = 0;  // group B: rows from (sr - k, tr) to (sr, tr)
 #pragma unroll
             for (int k = 0; k < WD; ++k) {
@@ -551,18 +567,21 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
 // recent rows the mids read.
 template <int WD, bool LO0>
 __global__ __launch_bounds__(64) void k_mid(DevChain ch, Tables tb, int32_t tau, int32_t accumulate,
-                                            int32_t n_chunks)
+                                            int32_t n_chunks, int32_t n_chunks_h)
 {
     constexpr int R = mid_rows<WD>();
     const int32_t n_blk = (ch.L - tau + R - 1) / R;
-    // per column chunk: group A's n_blk tiles, then group B's (lo > 0); gi indexes the group
+    // per column chunk: group A's n_blk tiles, then group B's (lo > 0); gi indexes the group.
+    // Chunks from n_chunks on are H's (the saving sweep).
     int32_t mc, rem;
     chunk_tile(blockIdx.x, (LO0 ? 1 : 2) * n_blk, &mc, &rem);
-    if (mc >= n_chunks) return;
+    if (mc >= n_chunks + n_chunks_h) return;
+    const bool hp = mc >= n_chunks;
+    if (hp) mc -= n_chunks;
     const int32_t gi = mc * n_blk + rem % n_blk;
-    if (LO0) mid_tile<WD, true, LO0>(ch, tb, tau, accumulate, gi);
-    else if (rem < n_blk) mid_tile<WD, true, false>(ch, tb, tau, accumulate, gi);
-    else mid_tile<WD, false, false>(ch, tb, tau, accumulate, gi);
+    if (LO0) mid_tile<WD, true, LO0>(ch, tb, tau, accumulate, gi, hp);
+    else if (rem < n_blk) mid_tile<WD, true, false>(ch, tb, tau, accumulate, gi, hp);
+    else mid_tile<WD, false, false>(ch, tb, tau, accumulate, gi, hp);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -595,10 +614,10 @@ __device__ inline int32_t ldrow(const int32_t *base, uint32_t pitch, uint32_t by
 }
 
 __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t d, int32_t midmin,
-                                                 int32_t n_chunks, int32_t n_run)
+                                                 int32_t n_chunks, int32_t n_run, int32_t n_chunks_h)
 {
     constexpr int32_t FB = 8, NC = FC / FT, NST = (HMAX + FC) / FT;
-    __shared__ int32_t seg[HMAX + FC];
+    __shared__ int32_t seg[HMAX + FC], seg3[HMAX + FC];
     const int32_t L = ch.L, K = ch.K, W = tb.W;
     // Tiles of one column chunk are adjacent in row s, and adjacent tiles run on one XCD: the
     // case-1 row (s+1, t) of a cell was written in the previous launch by the workgroup of
@@ -606,7 +625,10 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
     // fill, column chunks adjacent: 6.15 ms, no XCD-aware order: 6.7 ms).
     int32_t chunk, s;
     chunk_tile(blockIdx.x, (uint32_t)(L - d), &chunk, &s);
-    if (chunk >= n_chunks) return;
+    if (chunk >= n_chunks + n_chunks_h) return;
+    // chunks from n_chunks on finish H(s, t) of the saving sweep instead of Opt(s, t)
+    const bool hp = chunk >= n_chunks;
+    if (hp) chunk -= n_chunks;
     const int32_t t = s + d;
     const int32_t mbase = chunk * FC;
     const int32_t lane = (int32_t)(threadIdx.x & 63);
@@ -616,86 +638,104 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
     const int64_t stride = tb.stride;
     const uint32_t pitch = (uint32_t)stride * 4u;
     const int32_t padl = tb.padl;
-    int32_t *const orow = tb.opt + row_of(L, s, t) * stride + padl;  // column 0
+    const int64_t row_st = row_of(L, s, t);
+    int32_t *const orow = tb.opt + row_st * stride + padl;  // column 0
     const int32_t D = (d / midmin) * midmin;  // the products cover splits with max(a, b) < D
-    int32_t *const arow = tb.ap + row_of(L, s, t) * stride + padl;
     const int32_t ip = t + 1 < L ? s * L + t + 1 : 0;
+    // per-lane column offsets (past the last budget: the last one, computed and not stored)
+    uint32_t col[NC];  // byte offsets
+#pragma unroll
+    for (int c = 0; c < NC; ++c) col[c] = (uint32_t)min(ml + 64 * c, W - 1) * 4u;
+
+    // splits i0 .. i0+n-1: left(s, i-1) + Opt(i, t, m - x_i), left = ap (Opt) or aq read lsh
+    // columns to the left (H).  Pointers at column 0: row (s, i-1) is i-1-s rows after
+    // (s, s); Opt row (i+1, t) is L-1-i rows after (i, t)
+    int32_t best[NC];
+    auto splits = [&](const int32_t *ltab, int32_t lsh, int32_t i0, int32_t n) {
+        const int32_t *pa = ltab + (row_of(L, s, s) + (i0 - 1 - s)) * stride + padl - lsh;
+        const int32_t *pq = tb.opt + row_of(L, i0, t) * stride + padl;
+        int32_t i = i0;
+        for (int32_t j0 = 0; j0 < n; j0 += FB) {
+            int32_t va[FB][NC], vq[FB][NC];
+#pragma unroll
+            for (int u = 0; u < FB; ++u) {
+                if (j0 + u < n) {
+                    // a shift x_i > padl happens only when padl >= W: the read lands in the left pad
+                    const int32_t *const q = pq - min(ch.x[i], padl);
+#pragma unroll
+                    for (int c = 0; c < NC; ++c) {
+                        va[u][c] = ldrow(pa, pitch, col[c]);
+                        vq[u][c] = ldrow(q, pitch, col[c]);
+                    }
+                    pa += stride;
+                    pq += (int64_t)(L - 1 - i) * stride;
+                    ++i;
+                } else {
+#pragma unroll
+                    for (int c = 0; c < NC; ++c) {
+                        va[u][c] = DINF;
+                        vq[u][c] = 0;
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < FB; ++u)
+#pragma unroll
+                for (int c = 0; c < NC; ++c) best[c] = min(best[c], va[u][c] + vq[u][c]);
+        }
+    };
+    auto near_splits = [&](const int32_t *ltab, int32_t lsh) {
+        if (D == 0) {
+            splits(ltab, lsh, s + 1, d);
+        } else {
+            splits(ltab, lsh, s + 1, d - D);      // t - i >= D
+            splits(ltab, lsh, s + D + 1, d - D);  // i - 1 - s >= D
+        }
+    };
+
     // From budget msa(s,t) on, storing everything fits and Opt(s,t,m) = lb(s,t).  Chunks from
     // n_run on lie past the msa of every cell of the diagonal (the host's bound): they only
     // store.  The products and mids of these spans ran on at least the chunks below n_run.
-    // (The stores stay after every load on both paths, so the loads of the per-block and
+    // (The stores stay after every load on every path, so the loads of the per-block and
     // per-option arrays may use the scalar cache.)
-    int32_t best[NC];
-    if (chunk >= n_run) {
-        const int32_t lbv = ch.lb[row_of(L, s, t)];
+    if (hp) {
+        // H(s, t) = min_i aq(s, i, m - x_s) + Opt(i, t, m - x_i): the products' partial, then
+        // the near splits
+        const int32_t *const hrow = tb.hopt + row_st * stride + padl;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) best[c] = D > 0 ? ldb(hrow, col[c]) : DINF;
+        near_splits(tb.aq, min(ch.x[s], padl));
+    } else if (chunk >= n_run) {
+        const int32_t lbv = ch.lb[row_st];
 #pragma unroll
         for (int c = 0; c < NC; ++c) best[c] = lbv;
     } else {
-
-        // case-1 row, staged: column mbase - H + q at seg[q]
+        // the case-1 row Opt(s+1, t) and, with the saving sweep, the row H(s+1, t) of case 3,
+        // staged: column mbase - H + q at seg[q] (seg3[q])
         const int32_t H = ch.xbar_halo;
         const bool staged = d > 0 && H <= HMAX;
+        const bool sweep = ch.c3 != nullptr && d >= 2;
         const int32_t *const rest = d > 0 ? tb.opt + row_of(L, s + 1, t) * stride + padl : nullptr;
-        int32_t stv[NST];
+        const int32_t *const hrest = sweep ? tb.hopt + row_of(L, s + 1, t) * stride + padl : nullptr;
+        int32_t stv[NST], stv3[NST];
         if (staged) {
 #pragma unroll
             for (int k = 0; k < NST; ++k) {
                 const int32_t q = (int32_t)threadIdx.x + FT * k, c = mbase - H + q;
                 stv[k] = q < H + FC && c >= -padl ? rest[c] : DINF;
+                // H is read at m - mem >= 0 only (need1 >= mem): columns below 0 are never used
+                stv3[k] = sweep && q < H + FC && c >= 0 ? hrest[c] : DINF;
             }
         }
-
-        // per-lane column offsets (past the last budget: the last one, computed and not stored)
-        uint32_t col[NC];  // byte offsets
-#pragma unroll
-        for (int c = 0; c < NC; ++c) col[c] = (uint32_t)min(ml + 64 * c, W - 1) * 4u;
 #pragma unroll
         for (int c = 0; c < NC; ++c) best[c] = D > 0 ? ldb(orow, col[c]) : DINF;
+        near_splits(tb.ap, 0);
 
-        // splits i0 .. i0+n-1: ap(s, i-1) + Opt(i, t, m - x_i).  Pointers at column 0:
-        // ap row (s, i-1) is i-1-s rows after (s, s); Opt row (i+1, t) is L-1-i rows after (i, t)
-        auto splits = [&](int32_t i0, int32_t n) {
-            const int32_t *pa = tb.ap + (row_of(L, s, s) + (i0 - 1 - s)) * stride + padl;
-            const int32_t *pq = tb.opt + row_of(L, i0, t) * stride + padl;
-            int32_t i = i0;
-            for (int32_t j0 = 0; j0 < n; j0 += FB) {
-                int32_t va[FB][NC], vq[FB][NC];
-#pragma unroll
-                for (int u = 0; u < FB; ++u) {
-                    if (j0 + u < n) {
-                        // a shift x_i > padl happens only when padl >= W: the read lands in the left pad
-                        const int32_t *const q = pq - min(ch.x[i], padl);
-#pragma unroll
-                        for (int c = 0; c < NC; ++c) {
-                            va[u][c] = ldrow(pa, pitch, col[c]);
-                            vq[u][c] = ldrow(q, pitch, col[c]);
-                        }
-                        pa += stride;
-                        pq += (int64_t)(L - 1 - i) * stride;
-                        ++i;
-                    } else {
-#pragma unroll
-                        for (int c = 0; c < NC; ++c) {
-                            va[u][c] = DINF;
-                            vq[u][c] = 0;
-                        }
-                    }
-                }
-#pragma unroll
-                for (int u = 0; u < FB; ++u)
-#pragma unroll
-                    for (int c = 0; c < NC; ++c) best[c] = min(best[c], va[u][c] + vq[u][c]);
-            }
-        };
-        if (D == 0) {
-            splits(s + 1, d);
-        } else {
-            splits(s + 1, d - D);      // t - i >= D
-            splits(s + D + 1, d - D);  // i - 1 - s >= D
-        }
-
-        // case 1, option o: r(F_s^o) + r(B_s^o) + Opt(s+1,t,m-xbar), valid iff m >= need1[s][o]
+        // case 1, option o: r(F_s^o) + r(B_s^o) + Opt(s+1,t,m-xbar), valid iff m >= need1[s][o];
+        // case 3 (the saving sweep), option o: r(F)+r(B)+refwd + H(s+1,t,m-mem), same validity
         const int32_t *const c1 = ch.c1 + s * K, *const need1 = ch.need1 + s * K, *const xbar = ch.xbar + s * K;
+        const int32_t *const c3 = sweep ? ch.c3 + s * K : nullptr;
+        const int32_t x1 = ch.x[s + 1];
         if (d == 0) {
             for (int32_t o = 0; o < K; ++o)
 #pragma unroll
@@ -705,7 +745,10 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
 #pragma unroll
             for (int k = 0; k < NST; ++k) {
                 const int32_t q = (int32_t)threadIdx.x + FT * k;
-                if (q < H + FC) seg[q] = stv[k];
+                if (q < H + FC) {
+                    seg[q] = stv[k];
+                    if (sweep) seg3[q] = stv3[k];
+                }
             }
             __syncthreads();
             const int32_t *const sg = seg + H + (ml - mbase);  // column ml
@@ -723,24 +766,59 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
                         if (ml + 64 * c >= need1[o]) best[c] = min(best[c], c1[o] + so[64 * c]);
                 }
             }
+            if (sweep) {
+                const int32_t *const sg3 = seg3 + H + (ml - mbase);
+                for (int32_t o = 0; o < K; ++o) {
+                    const int32_t *const so = sg3 - (xbar[o] - x1);
+#pragma unroll
+                    for (int c = 0; c < NC; ++c)
+                        if (ml + 64 * c >= need1[o]) best[c] = min(best[c], c3[o] + so[64 * c]);
+                }
+            }
         } else {
             for (int32_t o = 0; o < K; ++o)
 #pragma unroll
                 for (int c = 0; c < NC; ++c)
                     if (ml + 64 * c >= need1[o]) best[c] = min(best[c], c1[o] + ldb(rest - xbar[o], col[c]));
+            if (sweep)
+                for (int32_t o = 0; o < K; ++o)
+#pragma unroll
+                    for (int c = 0; c < NC; ++c)
+                        if (ml + 64 * c >= need1[o])
+                            best[c] = min(best[c], c3[o] + ldb(hrest - (xbar[o] - x1), col[c]));
         }
     }
 
     // stores last: until here every scalar operand may come from the scalar cache
+    if (hp) {
+        int32_t *const hrow = tb.hopt + row_st * stride + padl;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            const int32_t m = ml + 64 * c;
+            if (m < W) hrow[m] = min(best[c], DINF);
+        }
+        return;
+    }
+    // Opt, the left operand ap(s, t+1) of Eq. fn and, with the saving sweep, the left operand
+    // aq(s, t+1, v) = P[s][t+1] + Opt(s, t, v) of H(s, .) if the sweep s..t fits v + x_s
+    int32_t *const arow = tb.ap + row_st * stride + padl;
+    int32_t *const qrow = tb.aq ? tb.aq + row_st * stride + padl : nullptr;
     const int32_t need2 = t + 1 < L ? ch.need2[ip] : 0, P = t + 1 < L ? ch.P[ip] : 0;
+    const int32_t need3 = qrow && t + 1 < L ? ch.need3[ip] : 0, xs = ch.x[s];
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
         const int32_t m = ml + 64 * c;
-        if (m < padl) orow[m - padl] = DINF;  // keep the left pad infinite
+        if (m < padl) {  // keep the left pads infinite
+            orow[m - padl] = DINF;
+            if (qrow) qrow[m - padl] = DINF;
+        }
         if (m < W) {
             const int32_t v = min(best[c], DINF);
             orow[m] = v;
-            if (t + 1 < L) arow[m] = m >= need2 ? min(P + v, DINF) : DINF;
+            if (t + 1 < L) {
+                arow[m] = m >= need2 ? min(P + v, DINF) : DINF;
+                if (qrow) qrow[m] = m + xs >= need3 ? min(P + v, DINF) : DINF;
+            }
         }
     }
 }
@@ -826,23 +904,28 @@ static hipError_t launch_mid(const DevChain &ch, const Tables &tb, hipStream_t s
     int32_t sat = 0;
     for (int32_t s = 0; s < L - d; ++s) sat = max(sat, ch.h_msa[row_of(L, s, min(s + d + WD - 1, L - 1))]);
     const int32_t n_chunks = min(n_mc, run_chunks(sat));
-    prof->work[KFILL_MID] += lo == 0 ? product_work(L, tb.W, d, WD, 0, WD, 0, WD)
-                                     : product_work(L, tb.W, d, WD, lo, d, 0, d) +
-                                           product_work(L, tb.W, d, WD, 0, lo, lo, d);
-    if (n_chunks == 0) return hipSuccess;  // every target cell is past msa: the finalize stores it
-    const dim3 grid(chunk_grid(n_chunks, (lo == 0 ? 1 : 2) * n_blk));
-    e = lo == 0 ? launch(prof, KFILL_MID, k_mid<WD, true>, grid, dim3(64), stream, ch, tb, d, 0, n_chunks)
-                : launch(prof, KFILL_MID, k_mid<WD, false>, grid, dim3(64), stream, ch, tb, d, 1, n_chunks);
+    const int32_t n_chunks_h = tb.hopt ? n_mc : 0;  // H of the saving sweep: every chunk
+    const int64_t w1 = lo == 0 ? product_work(L, tb.W, d, WD, 0, WD, 0, WD)
+                               : product_work(L, tb.W, d, WD, lo, d, 0, d) + product_work(L, tb.W, d, WD, 0, lo, lo, d);
+    prof->work[KFILL_MID] += w1 * (tb.hopt ? 2 : 1);
+    if (n_chunks + n_chunks_h == 0) return hipSuccess;  // every target cell is past msa: the finalize stores it
+    const dim3 grid(chunk_grid(n_chunks + n_chunks_h, (lo == 0 ? 1 : 2) * n_blk));
+    e = lo == 0 ? launch(prof, KFILL_MID, k_mid<WD, true>, grid, dim3(64), stream, ch, tb, d, 0, n_chunks, n_chunks_h)
+                : launch(prof, KFILL_MID, k_mid<WD, false>, grid, dim3(64), stream, ch, tb, d, 1, n_chunks,
+                         n_chunks_h);
     if (e != hipSuccess) return e;
     ++*n;
-    if (prof->on) {  // what runs: every tile on the launch's first n_chunks column chunks
-        auto run = [&](int32_t, int32_t) { return n_chunks; };
-        int64_t *w = &prof->eval[KFILL_MID], *by = &prof->bytes[KFILL_MID];
-        if (lo == 0) {
-            product_account(L, tb.W, d, WD, 0, WD, 0, WD, false, run, w, by);
-        } else {
-            product_account(L, tb.W, d, WD, lo, d, 0, d, true, run, w, by);
-            product_account(L, tb.W, d, WD, 0, lo, lo, d, true, run, w, by);
+    if (prof->on) {  // what runs: every tile on the launch's first n_chunks column chunks (H: all)
+        for (int32_t k : {n_chunks, n_chunks_h}) {
+            if (k == 0) continue;
+            auto run = [&](int32_t, int32_t) { return k; };
+            int64_t *w = &prof->eval[KFILL_MID], *by = &prof->bytes[KFILL_MID];
+            if (lo == 0) {
+                product_account(L, tb.W, d, WD, 0, WD, 0, WD, false, run, w, by);
+            } else {
+                product_account(L, tb.W, d, WD, lo, d, 0, d, true, run, w, by);
+                product_account(L, tb.W, d, WD, 0, lo, lo, d, true, run, w, by);
+            }
         }
     }
     return hipSuccess;
@@ -857,8 +940,8 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
     hipError_t e;
     int32_t n = 0;
     const int32_t midmin = fill_midmin(ch.L, tb.W);
-    e = launch(prof, KFILL_INIT, k_init_inf_rows, dim3((tb.stride + 255) / 256, 2 * (2 * SLACK + 1)), dim3(256),
-               stream, tb);
+    e = launch(prof, KFILL_INIT, k_init_inf_rows, dim3((tb.stride + 255) / 256, (tb.hopt ? 4 : 2) * (2 * SLACK + 1)),
+               dim3(256), stream, tb);
     if (e != hipSuccess) return e;
     ++n;
     const int32_t fin_x = (max(tb.W, tb.padl) + FC - 1) / FC;
@@ -869,19 +952,23 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
             for (int32_t s = 0; s < ch.L - d; ++s)
                 sat = max(sat, ch.h_msa[row_of(ch.L, s, min(s + d + BAND - 1, ch.L - 1))]);
             const int32_t n_chunks = min((tb.W + 63) / 64, run_chunks(sat));
-            prof->work[KFILL_PRODUCT] += product_work(ch.L, tb.W, d, BAND, 0, d, 0, d);
-            if (n_chunks > 0) {
-                const dim3 grid(chunk_grid(n_chunks, (ch.L - d + SW - 1) / SW));
+            const int32_t n_chunks_h = tb.hopt ? (tb.W + 63) / 64 : 0;  // H of the saving sweep: every chunk
+            prof->work[KFILL_PRODUCT] += product_work(ch.L, tb.W, d, BAND, 0, d, 0, d) * (tb.hopt ? 2 : 1);
+            if (n_chunks + n_chunks_h > 0) {
+                const dim3 grid(chunk_grid(n_chunks + n_chunks_h, (ch.L - d + SW - 1) / SW));
                 e = launch(prof, KFILL_PRODUCT, k_product<SR, TW, TH, NW>, grid, dim3(NW * 64), stream, ch, tb, d,
-                           n_chunks);
+                           n_chunks, n_chunks_h);
                 if (e != hipSuccess) return e;
                 ++n;
             }
-            if (prof->on) {  // every tile on the launch's first n_chunks column chunks
+            if (prof->on) {  // every tile on the launch's first n_chunks column chunks (H: all)
                 const int32_t L = ch.L;
-                auto tile = [&](int32_t, int32_t) { return n_chunks; };
-                product_account(L, tb.W, d, BAND, 0, d, 0, d, false, tile, &prof->eval[KFILL_PRODUCT],
-                                &prof->bytes[KFILL_PRODUCT]);
+                for (int32_t k : {n_chunks, n_chunks_h}) {
+                    if (k == 0) continue;
+                    auto tile = [&](int32_t, int32_t) { return k; };
+                    product_account(L, tb.W, d, BAND, 0, d, 0, d, false, tile, &prof->eval[KFILL_PRODUCT],
+                                    &prof->bytes[KFILL_PRODUCT]);
+                }
             }
         } else if (d % 16 == 0 && d > 0) {
             if ((e = launch_mid<16>(ch, tb, stream, d, &n, prof)) != hipSuccess) return e;
@@ -893,19 +980,24 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
         int32_t sat = 0;  // chunks from n_run on lie past every cell's msa: they only store
         for (int32_t s = 0; s + d < ch.L; ++s) sat = max(sat, ch.h_msa[row_of(ch.L, s, s + d)]);
         const int32_t n_run = (int32_t)std::min<int64_t>(fin_x, ((int64_t)sat + FC - 1) / FC);
-        e = launch(prof, KFILL_FINALIZE, k_finalize, dim3(chunk_grid(fin_x, ch.L - d)), dim3(FT), stream, ch, tb, d,
-                   midmin, fin_x, n_run);
+        const int32_t fin_h = tb.hopt && d >= 1 ? fin_x : 0;  // H(s, s+d) of the saving sweep
+        e = launch(prof, KFILL_FINALIZE, k_finalize, dim3(chunk_grid(fin_x + fin_h, ch.L - d)), dim3(FT), stream, ch,
+                   tb, d, midmin, fin_x, n_run, fin_h);
         if (e != hipSuccess) return e;
         ++n;
         const int32_t D = (d / midmin) * midmin, near = D > 0 ? 2 * (d - D) : d;
-        prof->work[KFILL_FINALIZE] += (int64_t)(ch.L - d) * (near + ch.K) * tb.W;
+        // per cell: Opt's near splits and options; with the sweep also H's near splits and
+        // case 3's options
+        const int64_t per_cell = near + ch.K + (tb.hopt ? near + (d >= 2 ? ch.K : 0) : 0);
+        prof->work[KFILL_FINALIZE] += (int64_t)(ch.L - d) * per_cell * tb.W;
         if (prof->on) {
             // per cell, in the workgroups below msa: two operand rows per split, the stored
             // partial, the case-1 row, the Opt row written; past msa only the Opt row
             // written; the ap row written where a later split uses it
             for (int32_t s = 0; s + d < ch.L; ++s) {
                 const int64_t run = std::min<int64_t>(tb.W, (int64_t)n_run * FC);
-                prof->eval[KFILL_FINALIZE] += run * (near + ch.K);
+                prof->eval[KFILL_FINALIZE] += run * (near + ch.K + (tb.hopt && d >= 2 ? ch.K : 0)) +
+                                              (tb.hopt ? (int64_t)tb.W * near : 0);
                 prof->bytes[KFILL_FINALIZE] +=
                     (run * (2 * near + (D > 0) + (d > 0) + 1) + (tb.W - run) + (s + d + 1 < ch.L ? tb.W : 0)) * 4;
             }
@@ -950,6 +1042,20 @@ __device__ inline uint64_t option_key(const DevChain &ch, const Tables &tb, int3
     return ((uint64_t)v << 32) | (uint32_t)(L + o);
 }
 
+// Case 3 (the saving sweep) with option slot o: code L + K + o.
+__device__ inline uint64_t sweep_key(const DevChain &ch, const Tables &tb, int32_t s, int32_t t,
+                                     int32_t m, int32_t o)
+{
+    const int32_t L = ch.L, K = ch.K;
+    if (!ch.c3 || t < s + 2 || m < ch.need1[s * K + o]) return ~0ull;
+    const int32_t mem = ch.xbar[s * K + o] - ch.x[s + 1];
+    const int32_t h = tb.hopt[row_of(L, s + 1, t) * tb.stride + tb.padl + (m - mem)];
+    if (h >= DINF) return ~0ull;
+    const int64_t v = (int64_t)ch.c3[s * K + o] + h;
+    if (v >= DINF) return ~0ull;
+    return ((uint64_t)v << 32) | (uint32_t)(L + K + o);
+}
+
 // One row of choice codes: thread m scans the candidates in code order.
 __global__ __launch_bounds__(256) void k_arg_row(DevChain ch, Tables tb, int32_t s, int32_t t,
                                                  int16_t *__restrict__ out)
@@ -959,6 +1065,8 @@ __global__ __launch_bounds__(256) void k_arg_row(DevChain ch, Tables tb, int32_t
     uint64_t best = ~0ull;
     for (int32_t i = s + 1; i <= t; ++i) best = min(best, split_key(ch, tb, s, t, m, i));
     for (int32_t o = 0; o < ch.K; ++o) best = min(best, option_key(ch, tb, s, t, m, o));
+    if (ch.c3)
+        for (int32_t o = 0; o < ch.K; ++o) best = min(best, sweep_key(ch, tb, s, t, m, o));
     out[m] = best == ~0ull ? (int16_t)-1 : (int16_t)(best & 0xffffu);
 }
 
@@ -998,6 +1106,9 @@ __device__ inline uint32_t wave_min_u32(uint32_t v)
 // are copied to LDS first, so no load waits on another.  Shifted columns are clamped into
 // the row's left pad: a candidate whose column would fall left of it is invalid.
 constexpr int32_t BT_XBAR_LDS_MAX = 8192;  // xbar entries kept in LDS (32 KiB)
+// Frames on the stack: every step pushes at most 2 per block its span loses (case 3 pushes
+// 4 and loses at least 2 blocks).
+__host__ __device__ inline int32_t bt_stack_cap(const DevChain &ch) { return (ch.c3 ? 4 : 2) * ch.L + 8; }
 
 template <bool XBAR_LDS>
 __global__ __launch_bounds__(64) void k_backtrace(DevChain ch, Tables tb, int32_t m_top,
@@ -1006,7 +1117,8 @@ __global__ __launch_bounds__(64) void k_backtrace(DevChain ch, Tables tb, int32_
 {
     extern __shared__ int32_t sh[];
     const int32_t lane = threadIdx.x, L = ch.L, K = ch.K;
-    const int32_t stack_cap = 2 * L + 8;
+    const int32_t stack_cap = bt_stack_cap(ch);
+    const bool sweep = ch.c3 != nullptr;
     Frame *const stk = reinterpret_cast<Frame *>(sh);
     int32_t *const xs = sh + 4 * stack_cap;  // x_0..x_L
     int32_t *const xbs = xs + (L + 1);
@@ -1080,6 +1192,11 @@ __global__ __launch_bounds__(64) void k_backtrace(DevChain ch, Tables tb, int32_
                 take(j < d, (uint32_t)av[u] + (uint32_t)qv[u], (uint32_t)(s + 1 + j));
             }
             take(o < K && m >= need, (uint32_t)c1 + (uint32_t)rest, (uint32_t)(L + o));
+            if (sweep) {  // case 3 with option o: c3 + H(s+1, t, m - mem), mem = xbar - x_{s+1}
+                const int32_t hv =
+                    tb.hopt[(uint64_t)rest_row * ustride + (uint32_t)(padl + max(m - (xb - xs[s + 1]), 0))];
+                take(o < K && m >= need && t >= s + 2, (uint32_t)ch.c3[ko] + (uint32_t)hv, (uint32_t)(L + K + o));
+            }
         }
         };
         if (d <= 64) cell(std::integral_constant<int, 1>{});
@@ -1091,8 +1208,42 @@ __global__ __launch_bounds__(64) void k_backtrace(DevChain ch, Tables tb, int32_
         const uint32_t code = wave_min_u32(bc == cost ? bk : ~0u);
         if (cost >= (uint32_t)DINF) { status = 1; break; }
         if ((int32_t)cost != own) { status = 2; break; }
-        if (sp + 2 > stack_cap) { status = 3; break; }
-        if (code >= (uint32_t)L) {
+        if (sp + 4 > stack_cap) { status = 3; break; }
+        if (code >= (uint32_t)(L + K)) {
+            // case 3: F_s^o keeps its data; the sweep s+1..i-1 to x_i, where i is H's choice at
+            // (s+1, t, u = m - mem); then i..t, x_i dropped, x_{s+1} made again from the kept
+            // data, s+1..i-1, and B_s^o
+            const int32_t o = (int32_t)code - L - K, s1 = s + 1;
+            const int32_t xb = xbar[s * K + o];
+            const int32_t u = m - (xb - xs[s1]);
+            const int32_t hown = tb.hopt[row_of(L, s1, t) * stride + padl + u];
+            const int32_t *const aq_s = tb.aq + (uint64_t)row32(s1, s1) * ustride + padl + u - min(xs[s1], padl);
+            uint64_t hb = ~0ull;
+            for (int32_t j = lane; j < t - s1; j += 64) {  // split i = s1 + 1 + j, code i
+                const int32_t i = s1 + 1 + j;
+                const int32_t a = aq_s[(uint64_t)(uint32_t)j * ustride];
+                const int32_t q = tb.opt[(uint64_t)row32(i, t) * ustride + (uint32_t)(padl + u - min(xs[i], padl))];
+                hb = min(hb, ((uint64_t)((uint32_t)a + (uint32_t)q) << 32) | (uint32_t)i);
+            }
+            const uint32_t hc = (uint32_t)(hb >> 32), hk = (uint32_t)hb;
+            const uint32_t hcost = wave_min_u32(hc);
+            const int32_t i = (int32_t)wave_min_u32(hc == hcost ? hk : ~0u);
+            if ((int32_t)hcost != hown || hcost >= (uint32_t)DINF || i <= s1 || i > t) { status = 2; break; }
+            emit(RK_FWD_SAVE, s, o);
+            for (int32_t k = lane; k < i - s - 1; k += 64) {
+                const int64_t at = n + 2 * (int64_t)k;
+                if (at < cap) ops[at] = rk_op{RK_FWD_NOSAVE, s1 + k, -1};
+                if (at + 1 < cap) ops[at + 1] = rk_op{RK_FREE_X, s1 + k, -1};
+            }
+            n += 2 * (int64_t)(i - s - 1);
+            push(Frame{1, RK_BWD, s, o});
+            push(Frame{0, s1, i - 1, m - xb});
+            push(Frame{1, RK_REFWD, s, o});
+            push(Frame{1, RK_FREE_X, i, -1});
+            have = true;
+            s = i;
+            m = u - xs[i];
+        } else if (code >= (uint32_t)L) {
             const int32_t o = (int32_t)code - L;
             emit(RK_FWD_SAVE, s, o);
             push(Frame{1, RK_BWD, s, o});
@@ -1127,7 +1278,7 @@ hipError_t launch_backtrace(const DevChain &ch, const Tables &tb, int32_t m_top,
                             int64_t cap, int64_t *res, hipStream_t stream)
 {
     const bool xbar_lds = (int64_t)ch.L * ch.K <= BT_XBAR_LDS_MAX;
-    const size_t lds = sizeof(Frame) * (size_t)(2 * ch.L + 8) + sizeof(int32_t) * (size_t)(ch.L + 1) +
+    const size_t lds = sizeof(Frame) * (size_t)bt_stack_cap(ch) + sizeof(int32_t) * (size_t)(ch.L + 1) +
                        (xbar_lds ? sizeof(int32_t) * (size_t)ch.L * ch.K : 0);
     if (xbar_lds)
         hipLaunchKernelGGL(k_backtrace<true>, dim3(1), dim3(64), lds, stream, ch, tb, m_top, ops, cap, res);

@@ -18,14 +18,14 @@ RK_INF = 2**31 - 1
 RK_TIME_LIMIT = (1 << 30) - 2
 RK_MAX_L = 2000
 RK_MAX_M = (1 << 26) - 2
-RK_FWD_NOSAVE, RK_FWD_SAVE, RK_BWD, RK_FREE_X = 0, 1, 2, 3
+RK_FWD_NOSAVE, RK_FWD_SAVE, RK_BWD, RK_FREE_X, RK_REFWD = 0, 1, 2, 3, 4
 (RK_OK, RK_E_INVAL, RK_E_OVERFLOW, RK_E_NOMEM, RK_E_DEVICE, RK_E_NOT_SOLVED, RK_E_INFEASIBLE,
  RK_E_BUFSZ, RK_E_INTERNAL) = 0, -1, -2, -3, -4, -5, -6, -7, -8
 
 EXPORTS = ("rk_chain_create", "rk_chain_destroy", "rk_workspace_bytes", "rk_solve", "rk_solve_async",
            "rk_result", "rk_extract_schedule", "rk_read_row", "rk_tradeoff_curve", "rk_last_fill_ms",
            "rk_set_profiling", "rk_set_option_pruning", "rk_chain_options",
-           "rk_fill_kernel_stats", "rk_strerror", "rk_solve_noalloc")
+           "rk_fill_kernel_stats", "rk_strerror", "rk_solve_noalloc", "rk_chain_set_saving_sweep")
 RK_NOALLOC_MAX_BYTES = 64 << 20
 
 
@@ -62,6 +62,7 @@ def load():
         lib.rk_solve.argtypes = [C.c_void_p, i32, i32p]
         lib.rk_solve_async.argtypes = [C.c_void_p, i32, C.c_void_p, C.c_size_t, C.c_void_p]
         lib.rk_solve_noalloc.argtypes = [C.c_void_p, i32, C.c_void_p]
+        lib.rk_chain_set_saving_sweep.argtypes = [C.c_void_p, i32p]
         lib.rk_result.argtypes = [C.c_void_p, i32p]
         lib.rk_extract_schedule.argtypes = [C.c_void_p, P(rk_op), i64, P(i64), P(i64)]
         lib.rk_read_row.argtypes = [C.c_void_p, i32, i32, i32p, P(C.c_int16)]
@@ -125,6 +126,16 @@ def rk_solve(h, M: int) -> int:
 def rk_solve_async(h, M: int, workspace_ptr: int, ws_bytes: int, stream_ptr: int | None) -> None:
     _check(load().rk_solve_async(h, int(M), C.c_void_p(workspace_ptr), C.c_size_t(ws_bytes),
                                  C.c_void_p(stream_ptr or 0)), "rk_solve_async")
+
+
+def rk_chain_set_saving_sweep(h, refwd) -> None:
+    """refwd: [L, K] re-forward times (the saving sweep on) or None (off)."""
+    if refwd is None:
+        _check(load().rk_chain_set_saving_sweep(h, None), "rk_chain_set_saving_sweep")
+    else:
+        a = _i32(refwd)
+        _check(load().rk_chain_set_saving_sweep(h, a.ctypes.data_as(C.POINTER(C.c_int32))),
+               "rk_chain_set_saving_sweep")
 
 
 def rk_solve_noalloc(h, M: int, stream_ptr: int | None = None) -> None:
@@ -213,6 +224,8 @@ class Solver:
         self.L, self.K = chain.L, chain.K
         self.h = rk_chain_create(chain.L, chain.K, *chain.arrays())
         self.M = None
+        if getattr(chain, "refwd", None) is not None:  # the saving sweep
+            rk_chain_set_saving_sweep(self.h, chain.refwd)
 
     def solve(self, M: int | None = None) -> int:
         self.M = self.chain.M if M is None else int(M)
@@ -230,6 +243,9 @@ class Solver:
 
     def schedule(self):
         return rk_extract_schedule(self.h)
+
+    def set_saving_sweep(self, refwd) -> None:
+        rk_chain_set_saving_sweep(self.h, refwd)
 
     def set_option_pruning(self, enable: bool) -> None:
         rk_set_option_pruning(self.h, enable)

@@ -1,5 +1,6 @@
 """The C ABI on a host without a GPU: the library loads, exports what include/rk.h
 declares, and rejects bad input before touching any device."""
+import ctypes as C
 import os
 import re
 
@@ -171,5 +172,39 @@ def test_reads_before_solve_are_refused():
         with pytest.raises(rk.RKError) as e:
             rk.rk_read_row(h, 0, ch.L, 10)
         assert e.value.code == rk.RK_E_INVAL
+    finally:
+        rk.rk_chain_destroy(h)
+
+
+def test_saving_sweep_arguments():
+    """rk_chain_set_saving_sweep: negative times and too many option codes are refused,
+    the time bound counts the re-forward, NULL switches the case off; the workspace of a
+    solve with the case on holds H and its left operand next to Opt and ap."""
+    ch = make_random_chain(3, 8, 2)
+    h = rk.rk_chain_create(*_args(ch))
+    try:
+        W0 = rk.rk_workspace_bytes(h, 100)
+        lib = rk.load()
+        bad = np.zeros((ch.L, ch.K), dtype=np.int32)
+        bad[2, 1] = -1
+        assert lib.rk_chain_set_saving_sweep(h, bad.ctypes.data_as(C.POINTER(C.c_int32))) == rk.RK_E_INVAL
+        big = np.full((ch.L, ch.K), rk.RK_TIME_LIMIT // (8 * 8) + 1, dtype=np.int32)
+        assert lib.rk_chain_set_saving_sweep(h, big.ctypes.data_as(C.POINTER(C.c_int32))) == rk.RK_E_OVERFLOW
+        assert rk.rk_workspace_bytes(h, 100) == W0  # unchanged after the refusals
+        ok = np.ones((ch.L, ch.K), dtype=np.int32)
+        rk.rk_chain_set_saving_sweep(h, ok)
+        assert rk.rk_workspace_bytes(h, 100) == 2 * W0
+        rk.rk_chain_set_saving_sweep(h, None)
+        assert rk.rk_workspace_bytes(h, 100) == W0
+        assert lib.rk_chain_set_saving_sweep(None, None) == rk.RK_E_INVAL
+    finally:
+        rk.rk_chain_destroy(h)
+    # codes up to L + 2K - 1 must fit int16
+    K = 16384  # L + K fits, L + 2K does not
+    wide = make_random_chain(4, 1, K)
+    h = rk.rk_chain_create(*_args(wide))
+    try:
+        ok = np.zeros((1, K), dtype=np.int32)
+        assert rk.load().rk_chain_set_saving_sweep(h, ok.ctypes.data_as(C.POINTER(C.c_int32))) == rk.RK_E_INVAL
     finally:
         rk.rk_chain_destroy(h)
