@@ -112,7 +112,7 @@ int rk_chain_set_saving_sweep(rk_chain *c, const int32_t *refwd);
 void rk_chain_destroy(rk_chain *c);
 
 /* Bytes of device workspace a solve of this chain at budget M needs (the
- * Opt table and its companions).  RK_E_INVAL for M outside [0, RK_MAX_M];
+ * Opt table over every span and every m <= M that Alg. 2 fills, and its companions).  RK_E_INVAL for M outside [0, RK_MAX_M];
  * RK_E_NOMEM when 18L + 64 table rows would span 2 GiB or more (the kernels
  * address operand blocks with 32-bit offsets; at L = 384 this allows budgets up
  * to about 77 000) or the tables exceed 2^40 int32. */
@@ -141,8 +141,11 @@ int rk_solve(rk_chain *c, int32_t M, int32_t *opt_out);
  * directly and become part of the caller's graph; nothing is allocated, uploaded or
  * waited on.  That needs a chain solved once before (outside the capture, with the
  * same option-pruning setting), a caller workspace, and profiling off, else
- * RK_E_INVAL.  Each replay of the caller's graph refills the table; rk_result and the
- * reads then return the last replay's results once it has run.
+ * RK_E_INVAL.  Each replay of the caller's graph refills the table.  The library
+ * cannot wait for the caller's replays: the caller synchronizes the stream it replays
+ * on before rk_result, rk_read_row, rk_tradeoff_curve or rk_extract_schedule, which then
+ * read the last replay's results without waiting; rk_last_fill_ms returns RK_E_INVAL
+ * for such a fill.  The same holds for rk_solve_noalloc on a stream under capture.
  */
 int rk_solve_async(rk_chain *c, int32_t M, void *d_workspace, size_t ws_bytes, void *stream);
 
@@ -185,7 +188,8 @@ int rk_result(rk_chain *c, int32_t *opt_out);
 int rk_extract_schedule(rk_chain *c, rk_op *ops, int64_t cap, int64_t *n_ops, int64_t *n_fwd);
 
 /*
- * Copy row (s,t) of the last solve: opt_row[m] = Opt(s,t,m) (RK_INF where
+ * Copy row (s,t) of the last solve: opt_row[m] = Opt(s,t,m), the optimal time of
+ * the span s..t within budget m (App. C, Eq. all; RK_INF where
  * infeasible) and arg_row[m] = the recorded choice code (-1 where infeasible),
  * for m = 0..M; each buffer holds M+1 entries and either may be NULL.
  * RK_E_INVAL unless 0 <= s <= t < L.

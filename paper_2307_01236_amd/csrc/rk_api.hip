@@ -35,6 +35,10 @@ struct rk_chain {
     bool queued = false;
 
     hipEvent_t ev_fill0 = nullptr, ev_fill1 = nullptr;
+    // The last fill went into a graph the caller is capturing: its events are not recorded
+    // (an event recorded inside a capture does not follow the graph's replays), reads do
+    // not wait, and no fill time is known.
+    bool in_caller_graph = false;
     int32_t launches = 0;
     rk::Profiler prof;
 
@@ -56,6 +60,13 @@ struct rk_chain {
     int16_t *d_argrow = nullptr;
     int32_t d_argrow_cap = 0;
 };
+
+// Wait for the last fill queued by the library.  A fill inside the caller's graph runs when
+// the caller replays it; the caller synchronizes before reading.
+static hipError_t wait_fill(rk_chain *c)
+{
+    return c->in_caller_graph ? hipSuccess : hipEventSynchronize(c->ev_fill1);
+}
 
 namespace {
 
@@ -112,7 +123,7 @@ int ensure_device(rk_chain *c)
 {
     if (c->d_chain && c->run_prune == c->prune && c->run_version == c->host_version) return RK_OK;
     if (c->d_chain) {  // rebuild: the captured launch sequence holds the old arrays
-        if (c->queued) HIPCHK(hipEventSynchronize(c->ev_fill1));
+        if (c->queued) HIPCHK(wait_fill(c));
         HIPCHK(hipFree(c->d_chain));
         c->d_chain = nullptr;
         if (c->gexec) (void)hipGraphExecDestroy(c->gexec);
@@ -218,7 +229,10 @@ int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t
     c->tb.hopt = c->dc.c3 ? c->tb.ap + tsz : nullptr;
     c->tb.aq = c->dc.c3 ? c->tb.ap + 2 * tsz : nullptr;
     c->stream = stream;
-    HIPCHK(hipEventRecord(c->ev_fill0, stream));
+    hipStreamCaptureStatus scs = hipStreamCaptureStatusNone;
+    HIPCHK(hipStreamIsCapturing(stream, &scs));
+    c->in_caller_graph = scs != hipStreamCaptureStatusNone;
+    if (!c->in_caller_graph) HIPCHK(hipEventRecord(c->ev_fill0, stream));
     const bool replay = c->gexec && c->g_M == M && c->g_tables == tables && c->g_stream == stream &&
                         c->g_prof == c->prof.on;
     if (direct) {
@@ -260,7 +274,7 @@ int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t
             HIPCHK(rk::launch_fill(c->dc, c->tb, stream, &c->launches, &c->prof));
         }
     }
-    HIPCHK(hipEventRecord(c->ev_fill1, stream));
+    if (!c->in_caller_graph) HIPCHK(hipEventRecord(c->ev_fill1, stream));
     c->queued = true;
     ++c->fills;
     return RK_OK;
@@ -269,7 +283,7 @@ int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t
 int answer(rk_chain *c, int32_t *out)
 {
     if (!c->queued) return RK_E_NOT_SOLVED;
-    HIPCHK(hipEventSynchronize(c->ev_fill1));
+    HIPCHK(wait_fill(c));
     if (c->M < c->h.x[0]) { *out = RK_INF; return RK_OK; }
     int32_t v = 0;
     const int64_t idx = rk::row_of(c->h.L, 0, c->h.L - 1) * c->tb.stride + c->tb.padl + (c->M - c->h.x[0]);
@@ -325,7 +339,7 @@ void rk_chain_destroy(rk_chain *c)
     if (!c) return;
     if (c->device >= 0) {  // something may live on the chain's device
         DeviceScope ds(c);
-        if (c->queued && c->ev_fill1) (void)hipEventSynchronize(c->ev_fill1);
+        if (c->queued && c->ev_fill1) (void)wait_fill(c);
         if (c->d_chain) (void)hipFree(c->d_chain);
         if (c->own_ws) (void)hipFree(c->own_ws);
         if (c->d_ops) (void)hipFree(c->d_ops);
@@ -368,7 +382,7 @@ int rk_solve_async(rk_chain *c, int32_t M, void *d_workspace, size_t ws_bytes, v
         return fill(c, M, g, static_cast<int32_t *>(d_workspace), static_cast<hipStream_t>(stream), true);
     }
     if ((rc = ensure_device(c)) != RK_OK) return rc;
-    if (c->queued) HIPCHK(hipEventSynchronize(c->ev_fill1));  // previous fill may still read its table
+    if (c->queued) HIPCHK(wait_fill(c));  // previous fill may still read its table
     int32_t *tab;
     if (d_workspace) {
         if (ws_bytes < need) return RK_E_NOMEM;
@@ -406,7 +420,7 @@ int rk_solve_noalloc(rk_chain *c, int32_t M, void *stream)
     if (!ds.ok) return RK_E_DEVICE;
     void *tab = nullptr;
     if ((rc = scratch_address(c->device, &tab)) != RK_OK) return rc;
-    if (c->queued) HIPCHK(hipEventSynchronize(c->ev_fill1));  // the previous fill may still read its table
+    if (c->queued) HIPCHK(wait_fill(c));  // the previous fill may still read its table
     // launched directly: capturing and instantiating a graph would allocate
     return fill(c, M, g, static_cast<int32_t *>(tab), stream ? static_cast<hipStream_t>(stream) : c->own_stream,
                 true);
@@ -479,7 +493,7 @@ int rk_read_row(rk_chain *c, int32_t s, int32_t t, int32_t *opt_row, int16_t *ar
     if (!c->queued) return RK_E_NOT_SOLVED;
     DeviceScope ds(c);
     if (!ds.ok) return RK_E_DEVICE;
-    HIPCHK(hipEventSynchronize(c->ev_fill1));
+    HIPCHK(wait_fill(c));
     const int64_t base = rk::row_of(c->h.L, s, t) * c->tb.stride + c->tb.padl;
     if (opt_row) {
         HIPCHK(hipMemcpy(opt_row, c->tb.opt + base, (size_t)c->W * sizeof(int32_t), hipMemcpyDeviceToHost));
@@ -514,7 +528,7 @@ int rk_tradeoff_curve(rk_chain *c, int32_t *times, int64_t n)
     if (n > (int64_t)c->W) return RK_E_INVAL;
     DeviceScope ds(c);
     if (!ds.ok) return RK_E_DEVICE;
-    HIPCHK(hipEventSynchronize(c->ev_fill1));
+    HIPCHK(wait_fill(c));
     // budget b leaves b - x_0 slots beyond the chain input: Opt(0, L-1, b - x_0)
     const int64_t x0 = c->h.x[0], lead = std::min<int64_t>(n, x0);
     for (int64_t b = 0; b < lead; ++b) times[b] = RK_INF;
@@ -532,6 +546,7 @@ int rk_last_fill_ms(rk_chain *c, float *ms, int32_t *launches)
     if (!c->queued) return RK_E_NOT_SOLVED;
     DeviceScope ds(c);
     if (!ds.ok) return RK_E_DEVICE;
+    if (c->in_caller_graph) return RK_E_INVAL;
     HIPCHK(hipEventSynchronize(c->ev_fill1));
     HIPCHK(hipEventElapsedTime(ms, c->ev_fill0, c->ev_fill1));
     if (launches) *launches = c->launches;
@@ -556,7 +571,7 @@ int rk_fill_kernel_stats(rk_chain *c, int32_t kind, int32_t *n_kinds, const char
     if (!c->queued) return RK_E_NOT_SOLVED;
     DeviceScope ds(c);
     if (!ds.ok) return RK_E_DEVICE;
-    HIPCHK(hipEventSynchronize(c->ev_fill1));
+    HIPCHK(wait_fill(c));
     int32_t cnt = 0;
     float sum = 0.f;
     for (int32_t j = 0; j < c->prof.n; ++j) {

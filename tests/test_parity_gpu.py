@@ -470,6 +470,12 @@ def test_fill_inside_a_torch_graph_capture():
                 assert np.array_equal(arg, o_arg)
             ops, nfwd = s.schedule()
             assert np.array_equal(ops, exp[0]) and nfwd == exp[1]
+        # a fill inside the caller's graph has no timing; an eager solve afterwards has
+        with pytest.raises(rk.RKError) as e:
+            s.fill_ms()
+        assert e.value.code == rk.RK_E_INVAL
+        s.solve_async(ch.M, ws.data_ptr(), nbytes, st.cuda_stream)
+        assert s.result() == sol.answer and s.fill_ms()[0] > 0
     finally:
         s.close()
 
