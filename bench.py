@@ -103,9 +103,9 @@ def cpu_baseline(ch, nblocks: int):
             "seconds": dt, "cpu_model": model, "host_cpus": os.cpu_count()}
 
 
-def extras(ch, s, M):
-    """Reports beside the benchmark: the trade-off curve against Rotor's, option pruning and
-    the fill of the smaller workloads."""
+def extras(ch, s, M, oracle_rate=None):
+    """Reports beside the benchmark: the trade-off curve against Rotor's, option pruning, the
+    smaller workloads and the saving sweep."""
     from paper_2307_01236_amd import rk
     from paper_2307_01236_amd.chaingen import make_grid_chain, relaxations
 
@@ -149,7 +149,11 @@ def extras(ch, s, M):
     log(f"option pruning: {pruning}")
 
     # the smaller workloads: fill time (captured launch sequence replayed, median of 5 after
-    # one warm-up), launches and relaxations per second; launch latency bounds the small ones
+    # one warm-up), launches and relaxations per second (launch latency bounds the small
+    # ones); the wall time of a synchronous solve (fill + answer) and of the schedule; the
+    # oracle's time for the whole chain on one host core where it takes seconds, else
+    # extrapolated from the oracle's measured rate on the benchmark sample
+    import oracle
     from paper_2307_01236_amd.chaingen import CONFIGS, make_config_chain
     others = []
     for cfg in range(len(CONFIGS)):
@@ -157,17 +161,47 @@ def extras(ch, s, M):
         if c.name == ch.name:
             continue
         cs = rk.Solver(c)
-        fills = []
+        fills, walls = [], []
         for _ in range(6):
+            t = time.perf_counter()
             cs.solve(c.M)
+            walls.append((time.perf_counter() - t) * 1e3)
             fills.append(cs.fill_ms()[0])
+        t = time.perf_counter()
+        cs.schedule()
+        sched = (time.perf_counter() - t) * 1e3
         ms = statistics.median(fills[1:])
-        others.append({"workload": c.name, "launches": cs.fill_ms()[1], "fill_ms": ms,
-                       "relaxations_per_s": relaxations(c.L, c.K, c.M) / (ms * 1e-3)})
+        r = relaxations(c.L, c.K, c.M)
+        row = {"workload": c.name, "launches": cs.fill_ms()[1], "fill_ms": ms, "relaxations_per_s": r / (ms * 1e-3),
+               "wall_solve_ms": statistics.median(walls[1:]), "schedule_ms": sched}
         cs.close()
+        if r <= 2e9 or oracle_rate is None:
+            t = time.perf_counter()
+            oracle.solve(c)
+            row["oracle_s"] = time.perf_counter() - t
+            row["oracle_kind"] = "measured, whole chain, one host core"
+        else:
+            row["oracle_s"] = r / oracle_rate
+            row["oracle_kind"] = "extrapolated from the benchmark sample's rate, one host core"
+        others.append(row)
     log(f"other workloads: {others}")
 
-    return tradeoff, pruning, others
+    # the saving sweep (the third case of the recurrence) on the benchmark chain: re-forward
+    # times drawn up to half a no-save forward; the fill carries the H tables beside Opt
+    from paper_2307_01236_amd.chaingen import with_refwd
+    sw = with_refwd(ch, 1, 0.0, 0.5)
+    ss = rk.Solver(sw)
+    fills = []
+    for _ in range(4):
+        ss.solve(M)
+        fills.append(ss.fill_ms()[0])
+    sweep = {"workload": sw.name, "M": M, "fill_ms": statistics.median(fills[1:]), "launches": ss.fill_ms()[1],
+             "answer": ss.result(), "answer_without": int(s.result()),
+             "schedule_refwd_ops": int((ss.schedule()[0][:, 0] == rk.RK_REFWD).sum())}
+    ss.close()
+    log(f"saving sweep: {sweep}")
+
+    return tradeoff, pruning, others, sweep
 
 
 def main():
@@ -273,9 +307,16 @@ def main():
     s.schedule()
     sched_ms = (time.perf_counter() - t) * 1e3
 
-    tradeoff = pruning = others = None
+    cpu = None
+    if args.cpu_blocks > 0:
+        log(f"cpu baseline: oracle on {args.cpu_blocks} blocks ...")
+        cpu = cpu_baseline(ch, min(args.cpu_blocks, ch.L))
+        cpu["whole_chain_s_extrapolated"] = relax / cpu["value"]
+        log(f"cpu baseline: {cpu['value']:.3e} relax/s ({cpu['seconds']:.1f} s)")
+
+    tradeoff = pruning = others = sweep = None
     if args.extras:  # other chains' fills: after the timed and profiled steps
-        tradeoff, pruning, others = extras(ch, s, M)
+        tradeoff, pruning, others, sweep = extras(ch, s, M, cpu["value"] if cpu else None)
 
     # dominant kernel: the one with the most device time; both of its roofs per launch
     dname, (dn, dms, _, dwork, dbytes) = max(kern.items(), key=lambda kv: kv[1][1])
@@ -294,9 +335,21 @@ def main():
     roofline.update({
         "traffic": traffic, "kernel": dname, "launches_per_step": dn / args.steps,
         "avg_launch_ms": dms / dn, "other_roof": other,
-        "whole_fill_valu_frac": OPS_PER_RELAX * relax / (statistics.median(fill_ms) * 1e-3) / 1e12
-                                / VALU_PEAK_TOPS,
+        "basis": "relaxations the kernel evaluates (candidates of cells below the budget from which "
+                 "storing everything fits are written in closed form, not evaluated)",
     })
+    # the whole fill against both roofs: every relaxation of the recurrence (nominal) and the
+    # ones the kernels evaluate, and the compulsory table traffic of all launches
+    fill_s = statistics.median(fill_ms) * 1e-3
+    evaluated = sum(v[3] for v in kern.values()) / args.steps
+    table_bytes = sum(v[4] for v in kern.values()) / args.steps
+    roofline["whole_fill"] = {
+        "fill_ms": fill_s * 1e3, "launches": sum(v[0] for v in kern.values()) / args.steps,
+        "relaxations_nominal": relax, "relaxations_evaluated": evaluated,
+        "valu_frac_nominal": OPS_PER_RELAX * relax / fill_s / 1e12 / VALU_PEAK_TOPS,
+        "valu_frac_evaluated": OPS_PER_RELAX * evaluated / fill_s / 1e12 / VALU_PEAK_TOPS,
+        "table_bytes": table_bytes, "hbm_frac_compulsory": table_bytes / fill_s / 1e9 / HBM_PEAK_GBS,
+    }
 
     # what this GPU sustains, next to the published peaks: int32 add+min chains over the
     # whole chip, a 1 GiB device copy (bytes read plus written) and a 1 GiB device read.
@@ -323,12 +376,6 @@ def main():
             r["measured_peak"] = measured["copy_gbs"]
         r["frac_of_measured"] = r["achieved"] / r["measured_peak"]
 
-    cpu = None
-    if args.cpu_blocks > 0:
-        log(f"cpu baseline: oracle on {args.cpu_blocks} blocks ...")
-        cpu = cpu_baseline(ch, min(args.cpu_blocks, ch.L))
-        log(f"cpu baseline: {cpu['value']:.3e} relax/s ({cpu['seconds']:.1f} s)")
-
     out = {
         "metric": METRIC, "value": relax / (ms_per_step * 1e-3), "unit": "relaxations/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
@@ -340,7 +387,7 @@ def main():
         "schedule_ms": sched_ms,
         "fill_relax_per_s": relax / (statistics.median(fill_ms) * 1e-3),
         "roofline": roofline, "measured_ceilings": measured, "cpu_baseline": cpu, "tradeoff": tradeoff,
-        "option_pruning": pruning, "other_workloads": others,
+        "option_pruning": pruning, "other_workloads": others, "saving_sweep": sweep,
         "kernels": {k: {"launches_per_step": v[0] / args.steps, "ms_per_step": v[1] / args.steps,
                         "relaxations_per_step": v[2] // args.steps, "evaluated_per_step": v[3] // args.steps,
                         "table_bytes_per_step": v[4] // args.steps}
