@@ -389,6 +389,25 @@ __device__ inline void static_for(F &&f)
 template <int WD>
 constexpr int mid_rows() { return 4; }
 
+// load at a byte offset from a wave-uniform base (one scalar base + one 32-bit lane offset)
+__device__ inline int32_t ldb(const int32_t *base, uint32_t byte_off)
+{
+    return *(const int32_t *)((const char *)base + byte_off);
+}
+
+// Maximum of a 32-bit value over the 64 lanes of a wavefront (all lanes active): DPP
+// exchanges inside each row of 16 lanes, then the four row maxima read as scalars.
+__device__ inline uint32_t wave_max_u32(uint32_t v)
+{
+    v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xb1, 0xf, 0xf, false));   // quad_perm 1,0,3,2
+    v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4e, 0xf, 0xf, false));   // quad_perm 2,3,0,1
+    v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x124, 0xf, 0xf, false));  // row_ror 4
+    v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x128, 0xf, 0xf, false));  // row_ror 8
+    const uint32_t r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
+    const uint32_t r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
+    return max(max(r0, r1), max(r2, r3));
+}
+
 template <int WD, bool GA, bool LO0>
 __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t tau, int32_t accumulate,
                                 int32_t g, bool hp)
@@ -443,6 +462,35 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
             xoff[j] = (uint32_t)rows_between(sa, max(sb + j, 0)) * pitch + col - lsh(max(sb + j, 0));
 #pragma unroll
         for (int r = 0; r < R; ++r) roff[r] = (uint32_t)r * pitch + col;
+    }
+
+    // Group A (lo > 0): every candidate of row s is at least lb(s,t) + P(s, s+lo+1).  A
+    // candidate of split i is ap(s,i) + Opt(i,t), ap(s,i) = P(s,i) + Opt(s,i-1), and
+    // Opt(s,i-1) + Opt(i,t) >= lb(s,i-1) + lb(i,t) = lb(s,t), the sum of the span's cheapest
+    // r(F)+r(B) (Opt of any span is at least its lb at every budget); P(s,i) grows with i and
+    // the tile's splits of row s start at s + lo + 1.  (With the saving sweep, H's candidates
+    // obey the same bound: aq holds the same P.)  When the stored partial of every cell and
+    // budget of the tile is already at most that bound, no candidate of the tile can lower
+    // it, and the tile is skipped.  The partial then holds the band product's and the wider
+    // mids' candidates, which at large spans already make the bound tight: long left spans
+    // cost a long recomputation sweep.  (A group B tile folding into the same cells at the
+    // same time only lowers the partial; any value it held bounds the final minimum.)
+    if (GA && !LO0) {
+        int32_t v = -DINF;
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int32_t s = base + r;
+            if (s < L - tau) {
+                const int32_t pm = ch.P[(int64_t)s * L + s + lo + 1];
+                const int32_t *const lbr = ch.lb + row_of(L, s, s + tau);
+                const int32_t *const pr = out + row_of(L, s, s + tau) * stride;
+#pragma unroll
+                for (int k = 0; k < WD; ++k)
+                    if (s + tau + k < L) v = max(v, ldb(pr + (int64_t)k * stride, col) - lbr[k] - pm);
+            }
+        }
+        if (m >= W) v = -DINF;
+        if ((int32_t)wave_max_u32((uint32_t)(v + DINF)) <= DINF) return;
     }
 
     // the shifts of the tile's splits, read once (a shift x_i > padl happens only when
@@ -599,11 +647,6 @@ __global__ __launch_bounds__(64) void k_mid(DevChain ch, Tables tb, int32_t tau,
 // ---------------------------------------------------------------------------------------
 constexpr int32_t FC = 128, FT = 64;  // budgets and threads per workgroup
 
-// load at a byte offset from a wave-uniform base (one scalar base + one 32-bit lane offset)
-__device__ inline int32_t ldb(const int32_t *base, uint32_t byte_off)
-{
-    return *(const int32_t *)((const char *)base + byte_off);
-}
 
 // the same through a buffer descriptor of one row (bytes [0, pitch) from base): the lane
 // offset goes to the load unchanged, with no per-lane address arithmetic
