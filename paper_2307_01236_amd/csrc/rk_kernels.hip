@@ -727,13 +727,19 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
                 for (int c = 0; c < NC; ++c) best[c] = min(best[c], va[u][c] + vq[u][c]);
         }
     };
-    auto near_splits = [&](const int32_t *ltab, int32_t lsh) {
-        if (D == 0) {
-            splits(ltab, lsh, s + 1, d);
-        } else {
-            splits(ltab, lsh, s + 1, d - D);      // t - i >= D
-            splits(ltab, lsh, s + D + 1, d - D);  // i - 1 - s >= D
-        }
+    // the near splits with a short left span (all of them when D == 0): t - i >= D
+    auto near_first = [&](const int32_t *ltab, int32_t lsh) { splits(ltab, lsh, s + 1, D == 0 ? d : d - D); };
+    // and those with a long left span, i - 1 - s >= D.  Each of their candidates is at least
+    // lb(s,t) + P(s, s+D+1) (ap(s,i) holds P(s,i) + Opt(s,i-1), Opt(s,i-1) + Opt(i,t) >= lb(s,t),
+    // and P grows with i; H's aq holds the same P): where the minimum so far is already at most
+    // that at every budget of the wave, they are skipped.
+    auto near_second = [&](const int32_t *ltab, int32_t lsh) {
+        if (D == 0 || d == D) return;
+        const int32_t bound = ch.lb[row_st] + ch.P[(int64_t)s * L + s + D + 1];
+        uint32_t over = 0;  // some lane's minimum is above the bound
+#pragma unroll
+        for (int c = 0; c < NC; ++c) over |= (uint32_t)(ml + 64 * c < W && best[c] > bound);
+        if (wave_max_u32(over)) splits(ltab, lsh, s + D + 1, d - D);
     };
 
     // From budget msa(s,t) on, storing everything fits and Opt(s,t,m) = lb(s,t).  Chunks from
@@ -747,7 +753,8 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
         const int32_t *const hrow = tb.hopt + row_st * stride + padl;
 #pragma unroll
         for (int c = 0; c < NC; ++c) best[c] = D > 0 ? ldb(hrow, col[c]) : DINF;
-        near_splits(tb.aq, min(ch.x[s], padl));
+        near_first(tb.aq, min(ch.x[s], padl));
+        near_second(tb.aq, min(ch.x[s], padl));
     } else if (chunk >= n_run) {
         const int32_t lbv = ch.lb[row_st];
 #pragma unroll
@@ -772,7 +779,7 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
         }
 #pragma unroll
         for (int c = 0; c < NC; ++c) best[c] = D > 0 ? ldb(orow, col[c]) : DINF;
-        near_splits(tb.ap, 0);
+        near_first(tb.ap, 0);
 
         // case 1, option o: r(F_s^o) + r(B_s^o) + Opt(s+1,t,m-xbar), valid iff m >= need1[s][o];
         // case 3 (the saving sweep), option o: r(F)+r(B)+refwd + H(s+1,t,m-mem), same validity
@@ -830,6 +837,7 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
                         if (ml + 64 * c >= need1[o])
                             best[c] = min(best[c], c3[o] + ldb(hrest - (xbar[o] - x1), col[c]));
         }
+        near_second(tb.ap, 0);  // after case 1 and case 3, whose minima tighten the bound test
     }
 
     // stores last: until here every scalar operand may come from the scalar cache
