@@ -138,6 +138,22 @@ static inline uint32_t chunk_grid(int32_t n_chunks, int32_t n_idx)
 // ---------------------------------------------------------------------------------------
 __device__ inline uint32_t sat_add(uint32_t a, uint32_t b) { return __builtin_elementwise_add_sat(a, b); }
 
+// Maximum of a 32-bit value over the 64 lanes of a wavefront (all lanes active): DPP
+// exchanges inside each row of 16 lanes, then the four row maxima read as scalars.
+__device__ inline uint32_t wave_max_u32(uint32_t v)
+{
+    v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xb1, 0xf, 0xf, false));   // quad_perm 1,0,3,2
+    v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4e, 0xf, 0xf, false));   // quad_perm 2,3,0,1
+    v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x124, 0xf, 0xf, false));  // row_ror 4
+    v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x128, 0xf, 0xf, false));  // row_ror 8
+    const uint32_t r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
+    const uint32_t r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
+    return max(max(r0, r1), max(r2, r3));
+}
+
+// Splits of the band product's first pass, before it cuts its split range (see k_product).
+constexpr int32_t PROD_PREFIX = 48;
+
 __device__ inline uint32_t buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff)
 {
     return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0);
@@ -273,78 +289,133 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
         }
     };
 
-    // Chunk order: neighbouring row blocks share most right operand rows at equal split i,
+    // Two passes over the splits.  A candidate of split i is at least lb(s,t) + P(s,i):
+    // ap(s,i) holds P(s,i) + Opt(s,i-1), and Opt(s,i-1) + Opt(i,t) >= lb(s,i-1) + lb(i,t) =
+    // lb(s,t), the sum of the span's cheapest r(F)+r(B) (Opt of any span is at least its lb at
+    // every budget); P(s,i) = F(i) - F(s) with F the prefix sums of r(F^0) (row 0 of P) grows
+    // with i.  The first pass takes the PROD_PREFIX splits from i_lo on, where every cell's
+    // cheapest splits lie; then the workgroup finds the first split i_cut at which
+    // F(i) >= acc - lb(s,t) + F(s) for every cell and budget, and the second pass takes only
+    // the splits below it: from there on no candidate can lower a partial minimum.
+    //
+    // Within a pass, neighbouring row blocks share most right operand rows at equal split i,
     // so the row blocks of a group start at one common split (anchor) and wrap around:
-    // [anchor, i_hi] in order, then [i_lo, anchor).  Their ranges differ by a shift only,
-    // so after the wrap they again visit equal i at about equal times, and the rows they
-    // share are read from L2 while still there.  (A chunk of the second part may run into
-    // the anchor: its splits are relaxed twice, which leaves the minimum unchanged.)
-    const int32_t gspan = (tau + 2 * SW - 2) / SW * SW;  // rows of a group
-    int32_t anchor = S0 / gspan * gspan + gspan - SW + 1;
-    if (anchor > i_hi) anchor = i_lo;
+    // [anchor, hi] in order, then [lo, anchor).  Their ranges differ by a shift only, so after
+    // the wrap they again visit equal i at about equal times, and the rows they share are read
+    // from L2 while still there.  (A chunk of the second part may run into the anchor: its
+    // splits are relaxed twice, which leaves the minimum unchanged.)  The first pass is short
+    // and ascends.
     constexpr int32_t DONE = 0x7fffffff;
-    auto next_chunk = [&](int32_t c) {
-        if (c >= anchor) return c + CI <= i_hi ? c + CI : (i_lo < anchor ? i_lo : DONE);
-        return c + CI < anchor ? c + CI : DONE;
+    auto pass = [&](int32_t lo, int32_t hi, int32_t anchor) {
+        auto next_chunk = [&](int32_t c) {
+            if (c >= anchor) return c + CI <= hi ? c + CI : (lo < anchor ? lo : DONE);
+            return c + CI < anchor ? c + CI : DONE;
+        };
+        seek(anchor);
+        fetch(anchor);
+        for (int32_t ic = anchor, buf = 0; ic != DONE; buf ^= 1) {
+            const int32_t inext = next_chunk(ic);
+            uint32_t *const qsb = qs + buf * QB;
+            const uint32_t *const qw = qsb + (rg * SR + kh) * 64 + lane;
+            // staged row jj*NW + wave of split ic + ii is final iff jj*NW - ii < qlim
+            const int32_t qlim = ic - S0 - wave;
+            if (qlim > (JW - 1) * NW) {
+#pragma unroll
+                for (int ii = 0; ii < CI; ++ii)
+#pragma unroll
+                    for (int jj = 0; jj < JW; ++jj) qsb[(ii * NQ + jj * NW + wave) * 64 + lane] = qv[ii][jj];
+            } else {
+#pragma unroll
+                for (int ii = 0; ii < CI; ++ii)
+#pragma unroll
+                    for (int jj = 0; jj < JW; ++jj)
+                        qsb[(ii * NQ + jj * NW + wave) * 64 + lane] = jj * NW - ii < qlim ? qv[ii][jj] : DINF;
+            }
+            // left operand of row r, split ic + ii is final iff r - ii > alim
+            const int32_t alim = ic - s0 - tau - 1;
+            uint32_t a[CI][SR];
+            if (alim + CI - 1 < 0) {
+#pragma unroll
+                for (int ii = 0; ii < CI; ++ii)
+#pragma unroll
+                    for (int r = 0; r < SR; ++r) a[ii][r] = av[ii][r];
+            } else {
+#pragma unroll
+                for (int ii = 0; ii < CI; ++ii)
+#pragma unroll
+                    for (int r = 0; r < SR; ++r) a[ii][r] = r - ii > alim ? av[ii][r] : DINF;
+            }
+            __syncthreads();
+            if (inext != DONE) {  // in flight while this chunk is relaxed
+                if (inext == ic + CI) {
+                    int32_t rows = 0;
+#pragma unroll
+                    for (int ii = 0; ii < CI; ++ii) rows += L - 1 - (ic + ii);
+                    qcur = (const int32_t *)((const char *)qcur + (int64_t)rows * pitch);
+                    acur = (const int32_t *)((const char *)acur + (int64_t)CI * pitch);
+                } else {
+                    seek(inext);
+                }
+                fetch(inext);
+            }
+            // acc(s0+r, s0+r+tau+k) = min(acc, ap(s0+r, i) + Opt(i, s0+r+tau+k, m - x_i)), two splits per min
+#pragma unroll
+            for (int ii = 0; ii < CI; ii += 2)
+#pragma unroll
+                for (int r = 0; r < SR; ++r)
+#pragma unroll
+                    for (int k = 0; k < TW; ++k)
+                        acc[r][k] = min(min(acc[r][k], sat_add(a[ii][r], qw[(ii * NQ + r + k) * 64])),
+                                        sat_add(a[ii + 1][r], qw[((ii + 1) * NQ + r + k) * 64]));
+            ic = inext;
+        }
     };
 
-    seek(anchor);
-    fetch(anchor);
-    for (int32_t ic = anchor, buf = 0; ic != DONE; buf ^= 1) {
-        const int32_t inext = next_chunk(ic);
-        uint32_t *const qsb = qs + buf * QB;
-        const uint32_t *const qw = qsb + (rg * SR + kh) * 64 + lane;
-        // staged row jj*NW + wave of split ic + ii is final iff jj*NW - ii < qlim
-        const int32_t qlim = ic - S0 - wave;
-        if (qlim > (JW - 1) * NW) {
+    const int32_t n_pre = min((i_hi - i_lo) / CI + 1, PROD_PREFIX / CI);  // chunks of the first pass
+    const int32_t lo2 = i_lo + CI * n_pre;                                // the second pass's first split
+    pass(i_lo, i_lo + CI * (n_pre - 1), i_lo);
+    if (lo2 <= i_hi) {
+        // the cut: the largest acc - lb(s,t) + F(s) over the wave's real cells and budgets
+        // (infinite partials keep every split), then over the workgroup through the staging
+        // buffer, which the first pass no longer reads
+        uint32_t thr = 0;
 #pragma unroll
-            for (int ii = 0; ii < CI; ++ii)
-#pragma unroll
-                for (int jj = 0; jj < JW; ++jj) qsb[(ii * NQ + jj * NW + wave) * 64 + lane] = qv[ii][jj];
-        } else {
-#pragma unroll
-            for (int ii = 0; ii < CI; ++ii)
-#pragma unroll
-                for (int jj = 0; jj < JW; ++jj)
-                    qsb[(ii * NQ + jj * NW + wave) * 64 + lane] = jj * NW - ii < qlim ? qv[ii][jj] : DINF;
-        }
-        // left operand of row r, split ic + ii is final iff r - ii > alim
-        const int32_t alim = ic - s0 - tau - 1;
-        uint32_t a[CI][SR];
-        if (alim + CI - 1 < 0) {
-#pragma unroll
-            for (int ii = 0; ii < CI; ++ii)
-#pragma unroll
-                for (int r = 0; r < SR; ++r) a[ii][r] = av[ii][r];
-        } else {
-#pragma unroll
-            for (int ii = 0; ii < CI; ++ii)
-#pragma unroll
-                for (int r = 0; r < SR; ++r) a[ii][r] = r - ii > alim ? av[ii][r] : DINF;
-        }
-        __syncthreads();
-        if (inext != DONE) {  // in flight while this chunk is relaxed
-            if (inext == ic + CI) {
-                int32_t rows = 0;
-#pragma unroll
-                for (int ii = 0; ii < CI; ++ii) rows += L - 1 - (ic + ii);
-                qcur = (const int32_t *)((const char *)qcur + (int64_t)rows * pitch);
-                acur = (const int32_t *)((const char *)acur + (int64_t)CI * pitch);
-            } else {
-                seek(inext);
-            }
-            fetch(inext);
-        }
-        // acc(s0+r, s0+r+tau+k) = min(acc, ap(s0+r, i) + Opt(i, s0+r+tau+k, m - x_i)), two splits per min
-#pragma unroll
-        for (int ii = 0; ii < CI; ii += 2)
-#pragma unroll
-            for (int r = 0; r < SR; ++r)
+        for (int r = 0; r < SR; ++r) {
+            const int32_t s = s0 + r;
+            if (s < s_end) {
+                const int32_t *const lbr = ch.lb + row_of(L, s, s + tau + kh);
+                const uint32_t fs = (uint32_t)ch.P[s];  // F(s) = P[0][s]
 #pragma unroll
                 for (int k = 0; k < TW; ++k)
-                    acc[r][k] = min(min(acc[r][k], sat_add(a[ii][r], qw[(ii * NQ + r + k) * 64])),
-                                    sat_add(a[ii + 1][r], qw[((ii + 1) * NQ + r + k) * 64]));
-        ic = inext;
+                    if (s + tau + kh + k < L)
+                        thr = max(thr, acc[r][k] >= (uint32_t)DINF ? 0xffffffffu : acc[r][k] - (uint32_t)lbr[k] + fs);
+            }
+        }
+        if (m >= (uint32_t)tb.W) thr = 0;
+        thr = wave_max_u32(thr);
+        __syncthreads();  // every wave is done with the staging buffers
+        if (lane == 0) qs[wave] = thr;
+        __syncthreads();
+#pragma unroll
+        for (int w = 0; w < NW; ++w) thr = max(thr, qs[w]);
+        thr = __builtin_amdgcn_readfirstlane(thr);
+        // i_cut: the first split i in [lo2, i_hi + 1) with F(i) >= thr (F is non-decreasing)
+        int32_t cl = lo2, ch_ = i_hi + 1;
+        if (thr != 0xffffffffu) {
+            while (cl < ch_) {
+                const int32_t mid = (cl + ch_) >> 1;
+                if ((uint32_t)ch.P[mid] >= thr) ch_ = mid;
+                else cl = mid + 1;
+            }
+        }
+        const int32_t hi2 = thr == 0xffffffffu ? i_hi : cl - 1;
+        if (lo2 <= hi2) {
+            const int32_t gspan = (tau + 2 * SW - 2) / SW * SW;  // rows of a group
+            int32_t anchor = S0 / gspan * gspan + gspan - SW + 1;
+            if (anchor > hi2 || anchor < lo2) anchor = lo2;
+            __syncthreads();  // the staging buffer held the thresholds
+            pass(lo2, hi2, anchor);
+        }
     }
     if (m >= (uint32_t)tb.W) return;
 #pragma unroll
@@ -393,19 +464,6 @@ constexpr int mid_rows() { return 4; }
 __device__ inline int32_t ldb(const int32_t *base, uint32_t byte_off)
 {
     return *(const int32_t *)((const char *)base + byte_off);
-}
-
-// Maximum of a 32-bit value over the 64 lanes of a wavefront (all lanes active): DPP
-// exchanges inside each row of 16 lanes, then the four row maxima read as scalars.
-__device__ inline uint32_t wave_max_u32(uint32_t v)
-{
-    v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xb1, 0xf, 0xf, false));   // quad_perm 1,0,3,2
-    v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4e, 0xf, 0xf, false));   // quad_perm 2,3,0,1
-    v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x124, 0xf, 0xf, false));  // row_ror 4
-    v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x128, 0xf, 0xf, false));  // row_ror 8
-    const uint32_t r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
-    const uint32_t r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
-    return max(max(r0, r1), max(r2, r3));
 }
 
 template <int WD, bool GA, bool LO0>
