@@ -214,27 +214,35 @@ int rk_tradeoff_curve(rk_chain *c, int32_t *times, int64_t n);
 int rk_last_fill_ms(rk_chain *c, float *ms, int32_t *launches);
 
 /*
- * Kernel-level timing (for benchmarks; off by default).  While enabled, the fill
- * launches its kernels one by one instead of replaying a graph, and the runtime
+ * Kernel-level timing (for benchmarks; mode 0, off, by default).  In mode 1 or 2 the
+ * fill launches its kernels one by one instead of replaying a graph, and the runtime
  * records a pair of HIP events with every dispatch, at the kernel's start and end
- * (hipExtLaunchKernelGGL), so a launch's time is the kernel's own.  rk_fill_kernel_stats
- * then reports, for kernel kind `kind` (0 <= kind < *n_kinds), its name as a profiler
- * shows it, the number of its launches in the last solve, their summed device time in
- * milliseconds, and three counts of the last profiled solve:
+ * (hipExtLaunchKernelGGL), so a launch's time is the kernel's own.  Mode 2 also runs
+ * the counting variants of the fill kernels, which add up on the device the candidates
+ * that only the kernels know to skip (slower: take timings from a mode-1 solve).
+ * rk_fill_kernel_stats then reports, for kernel kind `kind` (0 <= kind < *n_kinds), its
+ * name as a profiler shows it, the number of its launches in the last solve, their
+ * summed device time in milliseconds, and three counts of the last profiled solve:
  *   - relaxations: candidate evaluations of the recurrence the launches cover (valid
  *     (s,t,m,choice) combinations, with k_run option slots per block; see
  *     rk_chain_options);
  *   - evaluated: those the kernels actually evaluate.  Past the budget msa(s,t) from
  *     which storing every activation of span (s,t) fits, Opt(s,t,m) is known in closed
  *     form (the sum of its blocks' cheapest r(F)+r(B), App. C: Opt can never be lower,
- *     and case 1 with those options reaches it); tiles whose cells all lie there skip;
+ *     and case 1 with those options reaches it); tiles whose cells all lie there skip.
+ *     After a mode-2 solve, candidates skipped by a lower bound are left out as well:
+ *     every case-2 candidate of span (s,t) at split i costs at least lb(s,t) + P(s,i),
+ *     lb(s,t) being that closed form and P(s,i) the time of the plain forward sweep from
+ *     block s to block i-1 (the band products count what they relax; mids and finalizes,
+ *     what they skip);
  *   - bytes: compulsory table traffic of what runs: every table row a running tile
  *     reads, counted once over its budget columns, plus every row written (and read
  *     back where a fold into a stored partial happens).
  * Any output pointer may be NULL.  Waits for the last solve; timings and the last two
- * counts need profiling to have been on during it.  RK_E_INVAL for a kind out of range.
+ * counts need profiling to have been on during it.  RK_E_INVAL for a kind or mode out
+ * of range.
  */
-int rk_set_profiling(rk_chain *c, int32_t enable);
+int rk_set_profiling(rk_chain *c, int32_t mode);
 int rk_fill_kernel_stats(rk_chain *c, int32_t kind, int32_t *n_kinds, const char **name,
                          int32_t *launches, float *total_ms, int64_t *relaxations, int64_t *evaluated,
                          int64_t *bytes);

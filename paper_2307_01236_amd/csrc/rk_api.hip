@@ -228,6 +228,13 @@ int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t
     c->tb.ap = c->tb.opt + tsz;
     c->tb.hopt = c->dc.c3 ? c->tb.ap + tsz : nullptr;
     c->tb.aq = c->dc.c3 ? c->tb.ap + 2 * tsz : nullptr;
+    // profiled fills launch their kernels one by one, never inside a graph: with counting on,
+    // the counting variants of the kernels add what only they know (evaluated and skipped
+    // candidates) into a small device array
+    if (c->prof.count && !c->prof.d_ctr)
+        HIPCHK(hipMalloc(&c->prof.d_ctr, rk::CTR_WORDS * sizeof(unsigned long long)));
+    c->tb.ctr = c->prof.count ? c->prof.d_ctr : nullptr;
+    c->prof.ctr_valid = c->prof.count;
     c->stream = stream;
     hipStreamCaptureStatus scs = hipStreamCaptureStatusNone;
     HIPCHK(hipStreamIsCapturing(stream, &scs));
@@ -350,6 +357,7 @@ void rk_chain_destroy(rk_chain *c)
         if (c->ev_fill1) (void)hipEventDestroy(c->ev_fill1);
         if (c->own_stream) (void)hipStreamDestroy(c->own_stream);
         for (hipEvent_t e : c->prof.events) (void)hipEventDestroy(e);
+        if (c->prof.d_ctr) (void)hipFree(c->prof.d_ctr);
     }
     delete c;
 }
@@ -553,10 +561,11 @@ int rk_last_fill_ms(rk_chain *c, float *ms, int32_t *launches)
     return RK_OK;
 }
 
-int rk_set_profiling(rk_chain *c, int32_t enable)
+int rk_set_profiling(rk_chain *c, int32_t mode)
 {
-    if (!c) return RK_E_INVAL;
-    c->prof.on = enable != 0;
+    if (!c || mode < 0 || mode > 2) return RK_E_INVAL;
+    c->prof.on = mode != 0;
+    c->prof.count = mode == 2;
     return RK_OK;
 }
 
@@ -584,7 +593,22 @@ int rk_fill_kernel_stats(rk_chain *c, int32_t kind, int32_t *n_kinds, const char
     if (launches) *launches = cnt;
     if (total_ms) *total_ms = sum;
     if (relaxations) *relaxations = c->prof.work[kind];
-    if (evaluated) *evaluated = c->prof.eval[kind];
+    if (evaluated) {
+        // the host counts what each launch covers; the kernels report where the lower bound
+        // lb(s,t) + P(s,i) let them skip candidates
+        int64_t ev = c->prof.eval[kind];
+        if (c->prof.ctr_valid && c->prof.d_ctr &&
+            (kind == rk::KFILL_PRODUCT || kind == rk::KFILL_MID || kind == rk::KFILL_FINALIZE)) {
+            std::vector<unsigned long long> ctr(rk::CTR_WORDS);
+            HIPCHK(hipMemcpy(ctr.data(), c->prof.d_ctr, ctr.size() * sizeof ctr[0], hipMemcpyDeviceToHost));
+            const int32_t k = kind == rk::KFILL_PRODUCT ? 0 : kind == rk::KFILL_MID ? 1 : 2;
+            int64_t sum = 0;
+            for (int32_t j = 0; j < rk::CTR_SLOTS; ++j) sum += (int64_t)ctr[((int64_t)k * rk::CTR_SLOTS + j) * rk::CTR_PITCH];
+            if (k == 0) ev = sum;
+            else ev -= sum;
+        }
+        *evaluated = ev;
+    }
     if (bytes) *bytes = c->prof.bytes[kind];
     return RK_OK;
 }

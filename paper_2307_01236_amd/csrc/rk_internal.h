@@ -101,7 +101,18 @@ struct Tables {
     int32_t *aq;
     int32_t W, stride, padl;
     int64_t inf_row;  // index of the all-infinity row (= number of span rows)
+    // Profiled fills only (else null): candidate counts that only the kernels know, zeroed by
+    // the fill's first launch (layout: CTR_* below).
+    unsigned long long *ctr;
 };
+
+// The profiling counters: kind 0 counts the candidates the band products evaluate, kind 1
+// the mid candidates and kind 2 the finalize candidates skipped by the lower bound
+// lb(s,t) + P(s,i).  A workgroup adds into slot blockIdx.x % CTR_SLOTS of its kind, the slots
+// CTR_PITCH counters (128 bytes) apart, so that the atomics spread over the L2 channels
+// instead of queueing on one address; the host sums the slots.
+constexpr int32_t CTR_KINDS = 3, CTR_SLOTS = 256, CTR_PITCH = 16;
+constexpr int64_t CTR_WORDS = (int64_t)CTR_KINDS * CTR_SLOTS * CTR_PITCH;
 
 // Rows of one table in the workspace: slack, the span rows, the infinity row, slack.
 inline int64_t table_rows(int32_t L) { return (int64_t)L * (L + 1) / 2 + 1 + 2 * SLACK; }
@@ -117,6 +128,7 @@ inline int32_t round64(int64_t v) { return (int32_t)((v + 63) / 64 * 64); }
 // Optional per-launch event bracketing of the fill kernels (benchmark timing).
 struct Profiler {
     bool on = false;
+    bool count = false;  // also the device candidate counts (the kernels' counting variants)
     hipStream_t stream = nullptr;
     std::vector<hipEvent_t> events;  // pool, 2 per launch
     std::vector<int32_t> kinds;      // kernel kind of each bracketed launch
@@ -124,6 +136,8 @@ struct Profiler {
     int64_t work[8] = {};            // relaxations of the recurrence per kernel kind in the current solve
     int64_t eval[8] = {};            // relaxations evaluated (tiles past msa skip); profiling only
     int64_t bytes[8] = {};           // compulsory table traffic of what runs; profiling only
+    unsigned long long *d_ctr = nullptr;  // device counters of Tables::ctr (profiling only)
+    bool ctr_valid = false;               // the last fill was profiled: d_ctr holds its counts
     // two events from the pool for the next launch, which is of kind `kind`
     hipError_t slot(int32_t kind, hipEvent_t *start, hipEvent_t *stop);
     void reset(hipStream_t s)

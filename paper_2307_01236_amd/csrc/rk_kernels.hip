@@ -69,6 +69,8 @@ __global__ __launch_bounds__(256) void k_init_inf_rows(Tables tb)
     const int64_t row = k < SLACK ? (int64_t)k - SLACK : tb.inf_row + (k - SLACK);
     int32_t *const base = table == 0 ? tb.opt : table == 1 ? tb.ap : table == 2 ? tb.hopt : tb.aq;
     if (j < tb.stride) base[row * tb.stride + j] = DINF;
+    if (tb.ctr && blockIdx.x == 0 && y == 0)
+        for (int32_t k = (int32_t)threadIdx.x; k < CTR_KINDS * CTR_SLOTS; k += 256) tb.ctr[k * CTR_PITCH] = 0;
 }
 
 // ---------------------------------------------------------------------------------------
@@ -152,14 +154,20 @@ __device__ inline uint32_t wave_max_u32(uint32_t v)
 }
 
 // Splits of the band product's first pass, before it cuts its split range (see k_product).
-constexpr int32_t PROD_PREFIX = 48;
+constexpr int32_t PROD_PREFIX = 40;
+
+// profiling: add v to counter `kind` (one lane per wave calls it)
+__device__ inline void count(const Tables &tb, int32_t kind, int64_t v)
+{
+    atomicAdd(&tb.ctr[((int64_t)kind * CTR_SLOTS + blockIdx.x % CTR_SLOTS) * CTR_PITCH], (unsigned long long)v);
+}
 
 __device__ inline uint32_t buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff)
 {
     return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, (int)voff, (int)soff, 0);
 }
 
-template <int SR, int TW, int TH, int NW>
+template <int SR, int TW, int TH, int NW, bool CNT>
 __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int32_t tau, int32_t n_chunks,
                                                      int32_t n_chunks_h)
 {
@@ -303,8 +311,7 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
     // [anchor, hi] in order, then [lo, anchor).  Their ranges differ by a shift only, so after
     // the wrap they again visit equal i at about equal times, and the rows they share are read
     // from L2 while still there.  (A chunk of the second part may run into the anchor: its
-    // splits are relaxed twice, which leaves the minimum unchanged.)  The first pass is short
-    // and ascends.
+    // splits are relaxed twice, which leaves the minimum unchanged.)
     constexpr int32_t DONE = 0x7fffffff;
     auto pass = [&](int32_t lo, int32_t hi, int32_t anchor) {
         auto next_chunk = [&](int32_t c) {
@@ -372,8 +379,14 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
     };
 
     const int32_t n_pre = min((i_hi - i_lo) / CI + 1, PROD_PREFIX / CI);  // chunks of the first pass
+    int32_t e_last = min(i_hi, i_lo + CI * n_pre - 1);                      // the last split relaxed
     const int32_t lo2 = i_lo + CI * n_pre;                                // the second pass's first split
-    pass(i_lo, i_lo + CI * (n_pre - 1), i_lo);
+    // the first pass of the 4 row blocks of 32 rows: all start at the last block's first
+    // split, which lies in every one's first pass, and wrap around
+    const int32_t hi1 = i_lo + CI * (n_pre - 1);
+    int32_t anchor1 = S0 / (4 * SW) * (4 * SW) + 3 * SW + 1;
+    if (anchor1 < i_lo || anchor1 > hi1) anchor1 = i_lo;
+    pass(i_lo, hi1, anchor1);
     if (lo2 <= i_hi) {
         // the cut: the largest acc - lb(s,t) + F(s) over the wave's real cells and budgets
         // (infinite partials keep every split), then over the workgroup through the staging
@@ -415,7 +428,18 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
             if (anchor > hi2 || anchor < lo2) anchor = lo2;
             __syncthreads();  // the staging buffer held the thresholds
             pass(lo2, hi2, anchor);
+            e_last = min(i_hi, anchor + CI * ((hi2 - anchor) / CI) + CI - 1);
         }
+    }
+    if (CNT) {  // profiling: the candidates relaxed, splits i_lo..e_last of each real cell
+        int64_t n = 0;
+        for (int32_t r = 0; r < SR; ++r)
+            for (int32_t k = 0; k < TW; ++k) {
+                const int32_t s = s0 + r, t = s + tau + kh + k;
+                if (s < s_end && t < L) n += max(0, min(e_last, s + tau) - max(i_lo, t - tau + 1) + 1);
+            }
+        const int64_t cols = min(64, tb.W - (int32_t)mchunk * 64);
+        if (lane == 0) count(tb, 0, n * cols);
     }
     if (m >= (uint32_t)tb.W) return;
 #pragma unroll
@@ -466,7 +490,7 @@ __device__ inline int32_t ldb(const int32_t *base, uint32_t byte_off)
     return *(const int32_t *)((const char *)base + byte_off);
 }
 
-template <int WD, bool GA, bool LO0>
+template <int WD, bool GA, bool LO0, bool CNT>
 __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t tau, int32_t accumulate,
                                 int32_t g, bool hp)
 {
@@ -548,7 +572,17 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
             }
         }
         if (m >= W) v = -DINF;
-        if ((int32_t)wave_max_u32((uint32_t)(v + DINF)) <= DINF) return;
+        if ((int32_t)wave_max_u32((uint32_t)(v + DINF)) <= DINF) {
+            if (CNT) {  // profiling: the tile's candidates, WD per real cell
+                int64_t n = 0;
+                for (int32_t r = 0; r < R; ++r) {
+                    const int32_t s = base + r;
+                    if (s < L - tau) n += (int64_t)WD * min(WD, L - (s + tau));
+                }
+                if (lane == 0) count(tb, 1, n * min(64, W - mc * 64));
+            }
+            return;
+        }
     }
 
     // the shifts of the tile's splits, read once (a shift x_i > padl happens only when
@@ -671,7 +705,7 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
 // chunk by column chunk (group A's row blocks, then group B's), and consecutive tiles run
 // on one XCD: each XCD keeps the same range of columns as in the finalize launches, whose
 // recent rows the mids read.
-template <int WD, bool LO0>
+template <int WD, bool LO0, bool CNT>
 __global__ __launch_bounds__(64) void k_mid(DevChain ch, Tables tb, int32_t tau, int32_t accumulate,
                                             int32_t n_chunks, int32_t n_chunks_h)
 {
@@ -685,9 +719,9 @@ __global__ __launch_bounds__(64) void k_mid(DevChain ch, Tables tb, int32_t tau,
     const bool hp = mc >= n_chunks;
     if (hp) mc -= n_chunks;
     const int32_t gi = mc * n_blk + rem % n_blk;
-    if (LO0) mid_tile<WD, true, LO0>(ch, tb, tau, accumulate, gi, hp);
-    else if (rem < n_blk) mid_tile<WD, true, false>(ch, tb, tau, accumulate, gi, hp);
-    else mid_tile<WD, false, false>(ch, tb, tau, accumulate, gi, hp);
+    if (LO0) mid_tile<WD, true, LO0, CNT>(ch, tb, tau, accumulate, gi, hp);
+    else if (rem < n_blk) mid_tile<WD, true, false, CNT>(ch, tb, tau, accumulate, gi, hp);
+    else mid_tile<WD, false, false, CNT>(ch, tb, tau, accumulate, gi, hp);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -714,6 +748,7 @@ __device__ inline int32_t ldrow(const int32_t *base, uint32_t pitch, uint32_t by
     return __builtin_amdgcn_raw_buffer_load_b32(r, (int)byte_off, 0, 0);
 }
 
+template <bool CNT>
 __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t d, int32_t midmin,
                                                  int32_t n_chunks, int32_t n_run, int32_t n_chunks_h)
 {
@@ -798,6 +833,8 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
 #pragma unroll
         for (int c = 0; c < NC; ++c) over |= (uint32_t)(ml + 64 * c < W && best[c] > bound);
         if (wave_max_u32(over)) splits(ltab, lsh, s + D + 1, d - D);
+        else if (CNT && lane == 0)  // profiling: the skipped candidates
+            count(tb, 2, (int64_t)(d - D) * min(FC, W - mbase));
     };
 
     // From budget msa(s,t) on, storing everything fits and Opt(s,t,m) = lb(s,t).  Chunks from
@@ -1019,9 +1056,11 @@ static hipError_t launch_mid(const DevChain &ch, const Tables &tb, hipStream_t s
     prof->work[KFILL_MID] += w1 * (tb.hopt ? 2 : 1);
     if (n_chunks + n_chunks_h == 0) return hipSuccess;  // every target cell is past msa: the finalize stores it
     const dim3 grid(chunk_grid(n_chunks + n_chunks_h, (lo == 0 ? 1 : 2) * n_blk));
-    e = lo == 0 ? launch(prof, KFILL_MID, k_mid<WD, true>, grid, dim3(64), stream, ch, tb, d, 0, n_chunks, n_chunks_h)
-                : launch(prof, KFILL_MID, k_mid<WD, false>, grid, dim3(64), stream, ch, tb, d, 1, n_chunks,
-                         n_chunks_h);
+    const bool cnt = tb.ctr != nullptr;
+    e = lo == 0 ? launch(prof, KFILL_MID, cnt ? k_mid<WD, true, true> : k_mid<WD, true, false>, grid, dim3(64),
+                         stream, ch, tb, d, 0, n_chunks, n_chunks_h)
+                : launch(prof, KFILL_MID, cnt ? k_mid<WD, false, true> : k_mid<WD, false, false>, grid, dim3(64),
+                         stream, ch, tb, d, 1, n_chunks, n_chunks_h);
     if (e != hipSuccess) return e;
     ++*n;
     if (prof->on) {  // what runs: every tile on the launch's first n_chunks column chunks (H: all)
@@ -1065,8 +1104,8 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
             prof->work[KFILL_PRODUCT] += product_work(ch.L, tb.W, d, BAND, 0, d, 0, d) * (tb.hopt ? 2 : 1);
             if (n_chunks + n_chunks_h > 0) {
                 const dim3 grid(chunk_grid(n_chunks + n_chunks_h, (ch.L - d + SW - 1) / SW));
-                e = launch(prof, KFILL_PRODUCT, k_product<SR, TW, TH, NW>, grid, dim3(NW * 64), stream, ch, tb, d,
-                           n_chunks, n_chunks_h);
+                auto *const kp = tb.ctr ? k_product<SR, TW, TH, NW, true> : k_product<SR, TW, TH, NW, false>;
+                e = launch(prof, KFILL_PRODUCT, kp, grid, dim3(NW * 64), stream, ch, tb, d, n_chunks, n_chunks_h);
                 if (e != hipSuccess) return e;
                 ++n;
             }
@@ -1090,8 +1129,8 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
         for (int32_t s = 0; s + d < ch.L; ++s) sat = max(sat, ch.h_msa[row_of(ch.L, s, s + d)]);
         const int32_t n_run = (int32_t)std::min<int64_t>(fin_x, ((int64_t)sat + FC - 1) / FC);
         const int32_t fin_h = tb.hopt && d >= 1 ? fin_x : 0;  // H(s, s+d) of the saving sweep
-        e = launch(prof, KFILL_FINALIZE, k_finalize, dim3(chunk_grid(fin_x + fin_h, ch.L - d)), dim3(FT), stream, ch,
-                   tb, d, midmin, fin_x, n_run, fin_h);
+        e = launch(prof, KFILL_FINALIZE, tb.ctr ? k_finalize<true> : k_finalize<false>,
+                   dim3(chunk_grid(fin_x + fin_h, ch.L - d)), dim3(FT), stream, ch, tb, d, midmin, fin_x, n_run, fin_h);
         if (e != hipSuccess) return e;
         ++n;
         const int32_t D = (d / midmin) * midmin, near = D > 0 ? 2 * (d - D) : d;

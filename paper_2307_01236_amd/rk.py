@@ -196,8 +196,9 @@ def rk_chain_options(h, L: int, K: int):
     return kept.reshape(L, K).astype(bool), int(kr.value)
 
 
-def rk_set_profiling(h, enable: bool) -> None:
-    _check(load().rk_set_profiling(h, 1 if enable else 0), "rk_set_profiling")
+def rk_set_profiling(h, mode) -> None:
+    """mode: False/0 off, True/1 per-launch timing, 2 timing and the device candidate counts."""
+    _check(load().rk_set_profiling(h, int(mode)), "rk_set_profiling")
 
 
 def rk_fill_kernel_stats(h):
@@ -280,8 +281,8 @@ class Solver:
     def fill_ms(self):
         return rk_last_fill_ms(self.h)
 
-    def set_profiling(self, enable: bool) -> None:
-        rk_set_profiling(self.h, enable)
+    def set_profiling(self, mode) -> None:
+        rk_set_profiling(self.h, mode)
 
     def kernel_stats(self):
         return rk_fill_kernel_stats(self.h)

@@ -208,3 +208,19 @@ def test_saving_sweep_arguments():
         assert rk.load().rk_chain_set_saving_sweep(h, ok.ctypes.data_as(C.POINTER(C.c_int32))) == rk.RK_E_INVAL
     finally:
         rk.rk_chain_destroy(h)
+
+
+def test_profiling_modes():
+    """rk_set_profiling takes 0 (off), 1 (timing) and 2 (timing and device counts); other
+    modes and a NULL handle are refused."""
+    ch = make_config_chain(0)
+    h = rk.rk_chain_create(*_args(ch))
+    lib = rk.load()
+    try:
+        for mode in (1, 2, 0):
+            assert lib.rk_set_profiling(h, mode) == rk.RK_OK
+        for mode in (-1, 3):
+            assert lib.rk_set_profiling(h, mode) == rk.RK_E_INVAL
+        assert lib.rk_set_profiling(None, 1) == rk.RK_E_INVAL
+    finally:
+        rk.rk_chain_destroy(h)

@@ -289,6 +289,41 @@ def test_profiling_counts_launches():
         s.close()
 
 
+@pytest.mark.parametrize("cfg", [1, 2])
+def test_profiling_device_counts(cfg):
+    """Mode 2 runs the counting variants of the fill kernels: the same launches, results and
+    covered counts as mode 1, evaluated counts at most mode 1's (the lower bound only ever
+    skips), the same counts on a second solve (the counters restart with every fill), and
+    the answer the oracle's."""
+    ch = make_config_chain(cfg)
+    s = rk.Solver(ch)
+    try:
+        s.set_profiling(1)
+        a1 = s.solve()
+        st1 = s.kernel_stats()
+        s.set_profiling(2)
+        a2 = s.solve()
+        st2 = s.kernel_stats()
+        a3 = s.solve()
+        st3 = s.kernel_stats()
+        s.set_profiling(0)
+        assert a1 == a2 == a3 == oracle.solve(ch).answer
+        assert st1.keys() == st2.keys()
+        for name in st1:
+            n1, _, w1, e1, b1 = st1[name]
+            n2, _, w2, e2, b2 = st2[name]
+            assert (n1, w1, b1) == (n2, w2, b2), name
+            assert 0 <= e2 <= e1, (name, e1, e2)
+            assert (e2 > 0) == (e1 > 0), name
+            assert st3[name][3] == e2, name
+        # from span 64 on, a band product's split ranges pass its 40-split first pass and
+        # get cut: fewer candidates than its tiles cover
+        if ch.L > 64:
+            assert st2["k_product"][3] < st1["k_product"][3]
+    finally:
+        s.close()
+
+
 def test_graph_replays_match_oracle():
     """Repeated solves at one budget replay the captured launch sequence; each replay, with
     other solves and read-backs in between, must still match the oracle exactly."""
