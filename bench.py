@@ -14,7 +14,9 @@ kind with the most device time, from HIP events the runtime records with each
 dispatch on the solve's stream) against the roof that binds it: HBM bandwidth for its compulsory table
 traffic (every row a launch reads counted once, plus the rows it writes) or the
 VALU integer peak for its relaxations (an add and a min each), whichever
-fraction is higher; the other one is reported beside it; both are also priced
+fraction is higher, both counting only what the kernels evaluate (a profiled step
+with the counting kernel variants reports the candidates and rows that the lower
+bound lets them skip); the other one is reported beside it; both are also priced
 against what this GPU sustains (``measured_ceilings``: int32 add/min chains over
 the whole chip, a 1 GiB device copy and a 1 GiB device read; a kernel's bandwidth ceiling
 is the time-weighted mix of the read rate and the write rate the copy implies, for its own
@@ -288,19 +290,20 @@ def main():
     kern = {}
     for i in range(args.steps):
         step()
-        for name, (n, ms, work, _, moved) in s.kernel_stats().items():
+        for name, (n, ms, work, _, _) in s.kernel_stats().items():
             a = kern.setdefault(name, [0, 0.0, 0, 0, 0])
             a[0] += n
             a[1] += ms
             a[2] += work
-            a[4] += moved
     # one more step with the counting variants of the kernels (slower, not timed): the
-    # candidates each kind evaluates, net of what the lower bound lb(s,t) + P(s,i) skips;
-    # the fill is deterministic, so every step evaluates the same
+    # candidates each kind evaluates and the table rows they read, net of what the lower
+    # bound lb(s,t) + P(s,i) skips (the same in every step, up to the mid tiles whose
+    # bound test races with the folds of their launch's other tiles)
     s.set_profiling(2)
     step()
-    for name, (_, _, _, evaluated, _) in s.kernel_stats().items():
+    for name, (_, _, _, evaluated, moved) in s.kernel_stats().items():
         kern[name][3] = evaluated * args.steps
+        kern[name][4] = moved * args.steps
     s.set_profiling(0)
 
     # solve wall time without the schedule, warm (synchronous rk_solve on the library's table)
@@ -341,8 +344,9 @@ def main():
     roofline.update({
         "traffic": traffic, "kernel": dname, "launches_per_step": dn / args.steps,
         "avg_launch_ms": dms / dn, "other_roof": other,
-        "basis": "relaxations the kernel evaluates (candidates of cells below the budget from which "
-                 "storing everything fits are written in closed form, not evaluated)",
+        "basis": "relaxations the kernel evaluates and table rows it reads: candidates of cells past "
+                 "the budget from which storing everything fits are written in closed form, and those "
+                 "that the lower bound lb(s,t) + P(s,i) rules out are skipped (counted on the device)",
     })
     # the whole fill against both roofs: every relaxation of the recurrence (nominal) and the
     # ones the kernels evaluate, and the compulsory table traffic of all launches

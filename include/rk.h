@@ -237,7 +237,10 @@ int rk_last_fill_ms(rk_chain *c, float *ms, int32_t *launches);
  *     what they skip);
  *   - bytes: compulsory table traffic of what runs: every table row a running tile
  *     reads, counted once over its budget columns, plus every row written (and read
- *     back where a fold into a stored partial happens).
+ *     back where a fold into a stored partial happens).  After a mode-2 solve, only the
+ *     rows that the candidates left after the lower-bound skips read.  (A mid tile
+ *     tests its bound against partials that other tiles of its launch may be lowering at
+ *     that moment, so its counts can differ slightly from solve to solve.)
  * Any output pointer may be NULL.  Waits for the last solve; timings and the last two
  * counts need profiling to have been on during it.  RK_E_INVAL for a kind or mode out
  * of range.

@@ -234,6 +234,7 @@ int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t
     if (c->prof.count && !c->prof.d_ctr)
         HIPCHK(hipMalloc(&c->prof.d_ctr, rk::CTR_WORDS * sizeof(unsigned long long)));
     c->tb.ctr = c->prof.count ? c->prof.d_ctr : nullptr;
+    c->tb.rec = nullptr;  // the fill points it at the profiler's records per launch (mode 2)
     c->prof.ctr_valid = c->prof.count;
     c->stream = stream;
     hipStreamCaptureStatus scs = hipStreamCaptureStatusNone;
@@ -358,6 +359,7 @@ void rk_chain_destroy(rk_chain *c)
         if (c->own_stream) (void)hipStreamDestroy(c->own_stream);
         for (hipEvent_t e : c->prof.events) (void)hipEventDestroy(e);
         if (c->prof.d_ctr) (void)hipFree(c->prof.d_ctr);
+        if (c->prof.d_rec) (void)hipFree(c->prof.d_rec);
     }
     delete c;
 }
@@ -593,23 +595,16 @@ int rk_fill_kernel_stats(rk_chain *c, int32_t kind, int32_t *n_kinds, const char
     if (launches) *launches = cnt;
     if (total_ms) *total_ms = sum;
     if (relaxations) *relaxations = c->prof.work[kind];
-    if (evaluated) {
-        // the host counts what each launch covers; the kernels report where the lower bound
-        // lb(s,t) + P(s,i) let them skip candidates
-        int64_t ev = c->prof.eval[kind];
-        if (c->prof.ctr_valid && c->prof.d_ctr &&
-            (kind == rk::KFILL_PRODUCT || kind == rk::KFILL_MID || kind == rk::KFILL_FINALIZE)) {
-            std::vector<unsigned long long> ctr(rk::CTR_WORDS);
-            HIPCHK(hipMemcpy(ctr.data(), c->prof.d_ctr, ctr.size() * sizeof ctr[0], hipMemcpyDeviceToHost));
-            const int32_t k = kind == rk::KFILL_PRODUCT ? 0 : kind == rk::KFILL_MID ? 1 : 2;
-            int64_t sum = 0;
-            for (int32_t j = 0; j < rk::CTR_SLOTS; ++j) sum += (int64_t)ctr[((int64_t)k * rk::CTR_SLOTS + j) * rk::CTR_PITCH];
-            if (k == 0) ev = sum;
-            else ev -= sum;
-        }
-        *evaluated = ev;
+    // the finalize's skips (mode 2): candidates of near splits that the lower bound
+    // lb(s,t) + P(s,i) let a wave skip, each sparing two 4-byte operand reads
+    int64_t skipped = 0;
+    if (kind == rk::KFILL_FINALIZE && c->prof.ctr_valid && c->prof.d_ctr && (evaluated || bytes)) {
+        std::vector<unsigned long long> ctr(rk::CTR_WORDS);
+        HIPCHK(hipMemcpy(ctr.data(), c->prof.d_ctr, ctr.size() * sizeof ctr[0], hipMemcpyDeviceToHost));
+        for (int32_t j = 0; j < rk::CTR_SLOTS; ++j) skipped += (int64_t)ctr[(int64_t)j * rk::CTR_PITCH];
     }
-    if (bytes) *bytes = c->prof.bytes[kind];
+    if (evaluated) *evaluated = c->prof.eval[kind] - skipped;
+    if (bytes) *bytes = c->prof.bytes[kind] - 8 * skipped;
     return RK_OK;
 }
 

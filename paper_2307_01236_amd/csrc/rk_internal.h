@@ -101,18 +101,20 @@ struct Tables {
     int32_t *aq;
     int32_t W, stride, padl;
     int64_t inf_row;  // index of the all-infinity row (= number of span rows)
-    // Profiled fills only (else null): candidate counts that only the kernels know, zeroed by
-    // the fill's first launch (layout: CTR_* below).
+    // Profiling mode 2 only (else null).  ctr: the finalize candidates skipped by the lower
+    // bound lb(s,t) + P(s,i), zeroed by the fill's first launch (layout: CTR_* below).  rec:
+    // one entry per workgroup of the current product or mid launch (tile order of its grid):
+    // a band product's first split past the range it relaxed, a mid tile's 1 if it ran and
+    // 0 if its lower bound skipped it.
     unsigned long long *ctr;
+    int32_t *rec;
 };
 
-// The profiling counters: kind 0 counts the candidates the band products evaluate, kind 1
-// the mid candidates and kind 2 the finalize candidates skipped by the lower bound
-// lb(s,t) + P(s,i).  A workgroup adds into slot blockIdx.x % CTR_SLOTS of its kind, the slots
+// The finalize skip counter: a workgroup adds into slot blockIdx.x % CTR_SLOTS, the slots
 // CTR_PITCH counters (128 bytes) apart, so that the atomics spread over the L2 channels
 // instead of queueing on one address; the host sums the slots.
-constexpr int32_t CTR_KINDS = 3, CTR_SLOTS = 256, CTR_PITCH = 16;
-constexpr int64_t CTR_WORDS = (int64_t)CTR_KINDS * CTR_SLOTS * CTR_PITCH;
+constexpr int32_t CTR_SLOTS = 256, CTR_PITCH = 16;
+constexpr int64_t CTR_WORDS = (int64_t)CTR_SLOTS * CTR_PITCH;
 
 // Rows of one table in the workspace: slack, the span rows, the infinity row, slack.
 inline int64_t table_rows(int32_t L) { return (int64_t)L * (L + 1) / 2 + 1 + 2 * SLACK; }
@@ -136,10 +138,17 @@ struct Profiler {
     int64_t work[8] = {};            // relaxations of the recurrence per kernel kind in the current solve
     int64_t eval[8] = {};            // relaxations evaluated (tiles past msa skip); profiling only
     int64_t bytes[8] = {};           // compulsory table traffic of what runs; profiling only
-    unsigned long long *d_ctr = nullptr;  // device counters of Tables::ctr (profiling only)
-    bool ctr_valid = false;               // the last fill was profiled: d_ctr holds its counts
+    unsigned long long *d_ctr = nullptr;  // device counters of Tables::ctr (mode 2)
+    int32_t *d_rec = nullptr;             // Tables::rec (mode 2), room for rec_cap entries
+    int64_t rec_cap = 0;
+    std::vector<int32_t> h_rec;           // the last launch's records, read back
+    bool ctr_valid = false;               // the last fill counted: d_ctr holds its counts
     // two events from the pool for the next launch, which is of kind `kind`
     hipError_t slot(int32_t kind, hipEvent_t *start, hipEvent_t *stop);
+    // mode 2: room for n records of the next launch (waits for the stream before it grows)
+    hipError_t records(hipStream_t s, int64_t n);
+    // mode 2: the last launch's n records into h_rec (waits for the stream)
+    hipError_t read_records(hipStream_t s, int64_t n);
     void reset(hipStream_t s)
     {
         stream = s;

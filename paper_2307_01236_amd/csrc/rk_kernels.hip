@@ -38,6 +38,26 @@ hipError_t Profiler::slot(int32_t kind, hipEvent_t *start, hipEvent_t *stop)
     return hipSuccess;
 }
 
+hipError_t Profiler::records(hipStream_t s, int64_t n)
+{
+    if (n <= rec_cap) return hipSuccess;
+    hipError_t e = hipStreamSynchronize(s);  // the previous launch may still write the old buffer
+    if (e != hipSuccess) return e;
+    if (d_rec && (e = hipFree(d_rec)) != hipSuccess) return e;
+    d_rec = nullptr;
+    rec_cap = 0;
+    if ((e = hipMalloc(&d_rec, n * sizeof(int32_t))) != hipSuccess) return e;
+    rec_cap = n;
+    return hipSuccess;
+}
+
+hipError_t Profiler::read_records(hipStream_t s, int64_t n)
+{
+    h_rec.resize(n);
+    hipError_t e = hipMemcpyAsync(h_rec.data(), d_rec, n * sizeof(int32_t), hipMemcpyDeviceToHost, s);
+    return e != hipSuccess ? e : hipStreamSynchronize(s);
+}
+
 // Launch one fill kernel.  With profiling on, the runtime records a pair of events with the
 // dispatch itself (hipExtLaunchKernelGGL), at the kernel's start and end, so the elapsed
 // time is the kernel's own, without the gaps between launches.
@@ -70,7 +90,7 @@ __global__ __launch_bounds__(256) void k_init_inf_rows(Tables tb)
     int32_t *const base = table == 0 ? tb.opt : table == 1 ? tb.ap : table == 2 ? tb.hopt : tb.aq;
     if (j < tb.stride) base[row * tb.stride + j] = DINF;
     if (tb.ctr && blockIdx.x == 0 && y == 0)
-        for (int32_t k = (int32_t)threadIdx.x; k < CTR_KINDS * CTR_SLOTS; k += 256) tb.ctr[k * CTR_PITCH] = 0;
+        for (int32_t k = (int32_t)threadIdx.x; k < CTR_SLOTS; k += 256) tb.ctr[k * CTR_PITCH] = 0;
 }
 
 // ---------------------------------------------------------------------------------------
@@ -156,10 +176,10 @@ __device__ inline uint32_t wave_max_u32(uint32_t v)
 // Splits of the band product's first pass, before it cuts its split range (see k_product).
 constexpr int32_t PROD_PREFIX = 40;
 
-// profiling: add v to counter `kind` (one lane per wave calls it)
-__device__ inline void count(const Tables &tb, int32_t kind, int64_t v)
+// profiling: add v to the counter (one lane per wave calls it)
+__device__ inline void count(const Tables &tb, int64_t v)
 {
-    atomicAdd(&tb.ctr[((int64_t)kind * CTR_SLOTS + blockIdx.x % CTR_SLOTS) * CTR_PITCH], (unsigned long long)v);
+    atomicAdd(&tb.ctr[(int64_t)(blockIdx.x % CTR_SLOTS) * CTR_PITCH], (unsigned long long)v);
 }
 
 __device__ inline uint32_t buf_load(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff)
@@ -431,16 +451,8 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
             e_last = min(i_hi, anchor + CI * ((hi2 - anchor) / CI) + CI - 1);
         }
     }
-    if (CNT) {  // profiling: the candidates relaxed, splits i_lo..e_last of each real cell
-        int64_t n = 0;
-        for (int32_t r = 0; r < SR; ++r)
-            for (int32_t k = 0; k < TW; ++k) {
-                const int32_t s = s0 + r, t = s + tau + kh + k;
-                if (s < s_end && t < L) n += max(0, min(e_last, s + tau) - max(i_lo, t - tau + 1) + 1);
-            }
-        const int64_t cols = min(64, tb.W - (int32_t)mchunk * 64);
-        if (lane == 0) count(tb, 0, n * cols);
-    }
+    if (CNT && threadIdx.x == 0)  // profiling: every cell of the tile relaxed its splits i <= e_last
+        tb.rec[(int64_t)(hp ? n_chunks + chunk : chunk) * n_rb + rb] = e_last + 1;
     if (m >= (uint32_t)tb.W) return;
 #pragma unroll
     for (int r = 0; r < SR; ++r)
@@ -490,8 +502,10 @@ __device__ inline int32_t ldb(const int32_t *base, uint32_t byte_off)
     return *(const int32_t *)((const char *)base + byte_off);
 }
 
-template <int WD, bool GA, bool LO0, bool CNT>
-__device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t tau, int32_t accumulate,
+// Returns false when the tile is skipped by its lower bound.  Always inlined: k_mid calls it
+// from three places, and an outlined call would need a scratch frame.
+template <int WD, bool GA, bool LO0>
+__device__ __attribute__((always_inline)) inline bool mid_tile(const DevChain &ch, const Tables &tb, int32_t tau, int32_t accumulate,
                                 int32_t g, bool hp)
 {
     constexpr int R = mid_rows<WD>(), NS = WD + R - 1, NJ = R + WD - 1;
@@ -572,17 +586,7 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
             }
         }
         if (m >= W) v = -DINF;
-        if ((int32_t)wave_max_u32((uint32_t)(v + DINF)) <= DINF) {
-            if (CNT) {  // profiling: the tile's candidates, WD per real cell
-                int64_t n = 0;
-                for (int32_t r = 0; r < R; ++r) {
-                    const int32_t s = base + r;
-                    if (s < L - tau) n += (int64_t)WD * min(WD, L - (s + tau));
-                }
-                if (lane == 0) count(tb, 1, n * min(64, W - mc * 64));
-            }
-            return;
-        }
+        if ((int32_t)wave_max_u32((uint32_t)(v + DINF)) <= DINF) return false;
     }
 
     // the shifts of the tile's splits, read once (a shift x_i > padl happens only when
@@ -668,7 +672,7 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
     // store (or fold into the stored partial) through one descriptor per row r: group A
     // cell (s0+r, s0+r+tau+k) is k rows after (s0+r, s0+r+tau); group B cell
     // (t0+r-tau-k, t0+r) is sum_{s'=t0+r-tau-k}^{t0+r-tau-1} (L-1-s') rows before (t0+r-tau, t0+r)
-    if (m >= W) return;
+    if (m >= W) return true;
     const uint32_t cst = (uint32_t)(padl + m) * 4u;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
@@ -695,9 +699,8 @@ __device__ inline void mid_tile(const DevChain &ch, const Tables &tb, int32_t ta
             }
         }
     }
+    return true;
 }
-
-
 
 // One launch per level, one wavefront per workgroup and tile (single waves measured a
 // little faster than four-wave groups).  Groups A and B fold into the partials with atomic
@@ -719,9 +722,12 @@ __global__ __launch_bounds__(64) void k_mid(DevChain ch, Tables tb, int32_t tau,
     const bool hp = mc >= n_chunks;
     if (hp) mc -= n_chunks;
     const int32_t gi = mc * n_blk + rem % n_blk;
-    if (LO0) mid_tile<WD, true, LO0, CNT>(ch, tb, tau, accumulate, gi, hp);
-    else if (rem < n_blk) mid_tile<WD, true, false, CNT>(ch, tb, tau, accumulate, gi, hp);
-    else mid_tile<WD, false, false, CNT>(ch, tb, tau, accumulate, gi, hp);
+    bool ran;
+    if (LO0) ran = mid_tile<WD, true, LO0>(ch, tb, tau, accumulate, gi, hp);
+    else if (rem < n_blk) ran = mid_tile<WD, true, false>(ch, tb, tau, accumulate, gi, hp);
+    else ran = mid_tile<WD, false, false>(ch, tb, tau, accumulate, gi, hp);
+    // profiling: whether the tile ran or its lower bound skipped it
+    if (CNT && threadIdx.x == 0) tb.rec[(int64_t)(hp ? n_chunks + mc : mc) * ((LO0 ? 1 : 2) * n_blk) + rem] = ran;
 }
 
 // ---------------------------------------------------------------------------------------
@@ -834,7 +840,7 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
         for (int c = 0; c < NC; ++c) over |= (uint32_t)(ml + 64 * c < W && best[c] > bound);
         if (wave_max_u32(over)) splits(ltab, lsh, s + D + 1, d - D);
         else if (CNT && lane == 0)  // profiling: the skipped candidates
-            count(tb, 2, (int64_t)(d - D) * min(FC, W - mbase));
+            count(tb, (int64_t)(d - D) * min(FC, W - mbase));
     };
 
     // From budget msa(s,t) on, storing everything fits and Opt(s,t,m) = lb(s,t).  Chunks from
@@ -983,53 +989,74 @@ static int64_t product_work(int32_t L, int32_t W, int32_t tau, int32_t T, int32_
     return n * W;
 }
 
-// What a product launch does when it runs only some column chunks: chunks(s, t) = how many
-// 64-column chunks of cell (s,t)'s tile run.  Adds the relaxations evaluated and the
-// compulsory table traffic of the running tiles: per run of chunks with the same running tiles, the
-// distinct ap rows (s, s+a) and Opt rows (t-b, t) some real candidate of a running cell
-// reads, plus the target rows written (and read back when folding into a stored partial).
+// What a product launch does, column chunk by column chunk: cap(s, t, mc) = 0 when the tile
+// of cell (s, t) does not run on 64-column chunk mc, else the first split past those the
+// cell relaxes there (INT32_MAX: all of them).  Adds the relaxations evaluated and the
+// compulsory table traffic of what runs: per chunk, the distinct ap rows (s, s+a) and Opt
+// rows (t-b, t) some relaxed candidate reads, plus the target rows written (and read back
+// when folding into a stored partial).  Chunks whose cells run exactly as on the previous
+// chunk repeat its counts.
 template <class F>
-static void product_account(int32_t L, int32_t W, int32_t tau, int32_t T, int32_t alo, int32_t ahi,
-                            int32_t blo, int32_t bhi, bool accumulate, F chunks, int64_t *work, int64_t *bytes)
+static void tile_account(int32_t L, int32_t W, int32_t tau, int32_t T, int32_t alo, int32_t ahi, int32_t blo,
+                         int32_t bhi, bool accumulate, int32_t n_run, F cap, int64_t *work, int64_t *bytes)
 {
-    const int32_t n_mc = (W + 63) / 64, dmax = min(tau + T, L);
-    std::vector<int32_t> cuts{0};
-    for (int32_t dd = tau; dd < dmax; ++dd) {
-        int64_t c = 0;  // real splits of a cell of span dd
-        for (int32_t a = alo; a < min(ahi, dd); ++a) c += (dd - 1 - a >= blo && dd - 1 - a < bhi);
-        for (int32_t s = 0; s + dd < L; ++s) {
-            const int32_t k = min(chunks(s, s + dd), n_mc);
-            *work += c * min(W, 64 * k);
-            cuts.push_back(k);
-        }
-    }
-    std::sort(cuts.begin(), cuts.end());
-    cuts.erase(std::unique(cuts.begin(), cuts.end()), cuts.end());
-    for (size_t j = 1; j < cuts.size(); ++j) {
-        const int32_t c0 = cuts[j - 1], c1 = cuts[j];  // chunks [c0, c1) run the cells with chunks >= c1
-        const int64_t cols = min(W, 64 * c1) - 64 * c0;
-        if (cols <= 0) continue;
-        int64_t rows = 0;
-        for (int32_t s = 0; s < L - tau; ++s) {
-            int32_t lo = 0x7fffffff, hi = -1;
-            for (int32_t dd = tau; dd < min(dmax, L - s); ++dd) {
-                if (min(chunks(s, s + dd), n_mc) < c1) continue;
-                const int32_t a0 = max(alo, dd - bhi), a1 = min(ahi - 1, dd - 1 - blo);
-                if (a0 <= a1) lo = min(lo, a0), hi = max(hi, a1);
-                rows += accumulate ? 2 : 1;  // the target row written (and read back)
+    const int32_t dmax = min(tau + T, L);
+    std::vector<int32_t> caps, prev;
+    std::vector<std::pair<int32_t, int32_t>> iv;
+    int64_t c_work = 0, c_rows = 0;  // per column of the previous chunk
+    for (int32_t mc = 0; mc < n_run && 64 * mc < W; ++mc) {
+        caps.clear();
+        for (int32_t s = 0; s < L - tau; ++s)
+            for (int32_t dd = tau; dd < min(dmax, L - s); ++dd) caps.push_back(cap(s, s + dd, mc));
+        const int64_t cols = min(64, W - 64 * mc);
+        if (mc == 0 || caps != prev) {
+            c_work = c_rows = 0;
+            // split a of cell (s, s+dd) is real for a in [alo, ahi), b = dd-1-a in [blo, bhi), and
+            // relaxed for i = s+1+a < cap
+            auto arange = [&](int32_t s, int32_t dd, int32_t c, int32_t *a0, int32_t *a1) {
+                *a0 = max(alo, dd - bhi);
+                *a1 = min(min(ahi - 1, dd - 1 - blo), c == INT32_MAX ? INT32_MAX : c - 2 - s);
+            };
+            size_t q = 0;
+            for (int32_t s = 0; s < L - tau; ++s) {  // ap rows: the a intervals grow with dd
+                int32_t lo = 0, hi = -1;
+                for (int32_t dd = tau; dd < min(dmax, L - s); ++dd) {
+                    const int32_t c = caps[q++];
+                    if (c == 0) continue;
+                    c_rows += accumulate ? 2 : 1;  // the target row written (and read back)
+                    int32_t a0, a1;
+                    arange(s, dd, c, &a0, &a1);
+                    if (a0 > a1) continue;
+                    c_work += a1 - a0 + 1;
+                    if (hi < lo) lo = a0, hi = a1;
+                    else if (a0 <= hi + 1) hi = max(hi, a1);
+                    else c_rows += hi - lo + 1, lo = a0, hi = a1;
+                }
+                if (hi >= lo) c_rows += hi - lo + 1;
             }
-            if (hi >= lo) rows += hi - lo + 1;
-        }
-        for (int32_t t = tau; t < L; ++t) {
-            int32_t lo = 0x7fffffff, hi = -1;
-            for (int32_t dd = tau; dd < min(dmax, t + 1); ++dd) {
-                if (min(chunks(t - dd, t), n_mc) < c1) continue;
-                const int32_t b0 = max(blo, dd - ahi), b1 = min(bhi - 1, dd - 1 - alo);
-                if (b0 <= b1) lo = min(lo, b0), hi = max(hi, b1);
+            for (int32_t t = tau; t < L; ++t) {  // Opt rows: intervals of b, merged after sorting
+                iv.clear();
+                for (int32_t dd = tau; dd < min(dmax, t + 1); ++dd) {
+                    const int32_t s = t - dd;
+                    const int32_t c = cap(s, t, mc);
+                    if (c == 0) continue;
+                    int32_t a0, a1;
+                    arange(s, dd, c, &a0, &a1);
+                    if (a0 <= a1) iv.emplace_back(dd - 1 - a1, dd - 1 - a0);
+                }
+                std::sort(iv.begin(), iv.end());
+                int32_t lo = 0, hi = -1;
+                for (const auto &v : iv) {
+                    if (hi < lo) lo = v.first, hi = v.second;
+                    else if (v.first <= hi + 1) hi = max(hi, v.second);
+                    else c_rows += hi - lo + 1, lo = v.first, hi = v.second;
+                }
+                if (hi >= lo) c_rows += hi - lo + 1;
             }
-            if (hi >= lo) rows += hi - lo + 1;
+            prev.swap(caps);
         }
-        *bytes += rows * cols * 4;
+        *work += c_work * cols;
+        *bytes += c_rows * cols * 4;
     }
 }
 
@@ -1055,24 +1082,43 @@ static hipError_t launch_mid(const DevChain &ch, const Tables &tb, hipStream_t s
                                : product_work(L, tb.W, d, WD, lo, d, 0, d) + product_work(L, tb.W, d, WD, 0, lo, lo, d);
     prof->work[KFILL_MID] += w1 * (tb.hopt ? 2 : 1);
     if (n_chunks + n_chunks_h == 0) return hipSuccess;  // every target cell is past msa: the finalize stores it
-    const dim3 grid(chunk_grid(n_chunks + n_chunks_h, (lo == 0 ? 1 : 2) * n_blk));
+    const int32_t n_groups = lo == 0 ? 1 : 2;
+    const dim3 grid(chunk_grid(n_chunks + n_chunks_h, n_groups * n_blk));
     const bool cnt = tb.ctr != nullptr;
+    const int64_t n_rec = (int64_t)(n_chunks + n_chunks_h) * n_groups * n_blk;
+    Tables tr = tb;
+    if (cnt) {
+        if ((e = prof->records(stream, n_rec)) != hipSuccess) return e;
+        tr.rec = prof->d_rec;
+    }
     e = lo == 0 ? launch(prof, KFILL_MID, cnt ? k_mid<WD, true, true> : k_mid<WD, true, false>, grid, dim3(64),
-                         stream, ch, tb, d, 0, n_chunks, n_chunks_h)
+                         stream, ch, tr, d, 0, n_chunks, n_chunks_h)
                 : launch(prof, KFILL_MID, cnt ? k_mid<WD, false, true> : k_mid<WD, false, false>, grid, dim3(64),
-                         stream, ch, tb, d, 1, n_chunks, n_chunks_h);
+                         stream, ch, tr, d, 1, n_chunks, n_chunks_h);
     if (e != hipSuccess) return e;
     ++*n;
-    if (prof->on) {  // what runs: every tile on the launch's first n_chunks column chunks (H: all)
-        for (int32_t k : {n_chunks, n_chunks_h}) {
+    if (prof->on) {
+        // what runs: every tile on the launch's first n_chunks column chunks (H: all); with the
+        // records, only the tiles that ran.  A group A tile holds the cells of R rows, a group
+        // B tile those of R ends.
+        if (cnt && (e = prof->read_records(stream, n_rec)) != hipSuccess) return e;
+        for (int32_t part = 0; part < 2; ++part) {  // Opt's chunks, then H's
+            const int32_t k = part ? n_chunks_h : n_chunks, c0 = part ? n_chunks : 0;
             if (k == 0) continue;
-            auto run = [&](int32_t, int32_t) { return k; };
+            auto cap = [&](int32_t grp) {
+                return [&, grp](int32_t s, int32_t t, int32_t mc) -> int32_t {
+                    if (mc >= k) return 0;
+                    if (!cnt) return INT32_MAX;
+                    const int32_t blk = grp == 0 ? s / R : (t - d) / R;
+                    return prof->h_rec[((int64_t)(c0 + mc) * n_groups + grp) * n_blk + blk] ? INT32_MAX : 0;
+                };
+            };
             int64_t *w = &prof->eval[KFILL_MID], *by = &prof->bytes[KFILL_MID];
             if (lo == 0) {
-                product_account(L, tb.W, d, WD, 0, WD, 0, WD, false, run, w, by);
+                tile_account(L, tb.W, d, WD, 0, WD, 0, WD, false, k, cap(0), w, by);
             } else {
-                product_account(L, tb.W, d, WD, lo, d, 0, d, true, run, w, by);
-                product_account(L, tb.W, d, WD, 0, lo, lo, d, true, run, w, by);
+                tile_account(L, tb.W, d, WD, lo, d, 0, d, true, k, cap(0), w, by);
+                tile_account(L, tb.W, d, WD, 0, lo, lo, d, true, k, cap(1), w, by);
             }
         }
     }
@@ -1102,20 +1148,34 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
             const int32_t n_chunks = min((tb.W + 63) / 64, run_chunks(sat));
             const int32_t n_chunks_h = tb.hopt ? (tb.W + 63) / 64 : 0;  // H of the saving sweep: every chunk
             prof->work[KFILL_PRODUCT] += product_work(ch.L, tb.W, d, BAND, 0, d, 0, d) * (tb.hopt ? 2 : 1);
+            const int32_t n_rb = (ch.L - d + SW - 1) / SW;  // row blocks: a workgroup holds SW rows
+            const bool cnt = tb.ctr != nullptr;
+            const int64_t n_rec = (int64_t)(n_chunks + n_chunks_h) * n_rb;
             if (n_chunks + n_chunks_h > 0) {
-                const dim3 grid(chunk_grid(n_chunks + n_chunks_h, (ch.L - d + SW - 1) / SW));
-                auto *const kp = tb.ctr ? k_product<SR, TW, TH, NW, true> : k_product<SR, TW, TH, NW, false>;
-                e = launch(prof, KFILL_PRODUCT, kp, grid, dim3(NW * 64), stream, ch, tb, d, n_chunks, n_chunks_h);
+                const dim3 grid(chunk_grid(n_chunks + n_chunks_h, n_rb));
+                auto *const kp = cnt ? k_product<SR, TW, TH, NW, true> : k_product<SR, TW, TH, NW, false>;
+                Tables tr = tb;
+                if (cnt) {
+                    if ((e = prof->records(stream, n_rec)) != hipSuccess) return e;
+                    tr.rec = prof->d_rec;
+                }
+                e = launch(prof, KFILL_PRODUCT, kp, grid, dim3(NW * 64), stream, ch, tr, d, n_chunks, n_chunks_h);
                 if (e != hipSuccess) return e;
                 ++n;
+                if (cnt && (e = prof->read_records(stream, n_rec)) != hipSuccess) return e;
             }
-            if (prof->on) {  // every tile on the launch's first n_chunks column chunks (H: all)
-                const int32_t L = ch.L;
-                for (int32_t k : {n_chunks, n_chunks_h}) {
+            if (prof->on) {
+                // every tile on the launch's first n_chunks column chunks (H: all), relaxing all
+                // its splits or, with the records, those below the recorded one
+                for (int32_t part = 0; part < 2; ++part) {  // Opt's chunks, then H's
+                    const int32_t k = part ? n_chunks_h : n_chunks, c0 = part ? n_chunks : 0;
                     if (k == 0) continue;
-                    auto tile = [&](int32_t, int32_t) { return k; };
-                    product_account(L, tb.W, d, BAND, 0, d, 0, d, false, tile, &prof->eval[KFILL_PRODUCT],
-                                    &prof->bytes[KFILL_PRODUCT]);
+                    auto cap = [&](int32_t s, int32_t, int32_t mc) -> int32_t {
+                        if (mc >= k) return 0;
+                        return cnt ? prof->h_rec[(int64_t)(c0 + mc) * n_rb + s / SW] : INT32_MAX;
+                    };
+                    tile_account(ch.L, tb.W, d, BAND, 0, d, 0, d, false, k, cap, &prof->eval[KFILL_PRODUCT],
+                                 &prof->bytes[KFILL_PRODUCT]);
                 }
             }
         } else if (d % 16 == 0 && d > 0) {
@@ -1141,13 +1201,16 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
         if (prof->on) {
             // per cell, in the workgroups below msa: two operand rows per split, the stored
             // partial, the case-1 row, the Opt row written; past msa only the Opt row
-            // written; the ap row written where a later split uses it
+            // written; the ap row written where a later split uses it.  With the saving
+            // sweep, H's workgroups (every column, d >= 1): two operand rows per split, the
+            // stored partial and the H row written.
             for (int32_t s = 0; s + d < ch.L; ++s) {
                 const int64_t run = std::min<int64_t>(tb.W, (int64_t)n_run * FC);
                 prof->eval[KFILL_FINALIZE] += run * (near + ch.K + (tb.hopt && d >= 2 ? ch.K : 0)) +
                                               (tb.hopt ? (int64_t)tb.W * near : 0);
                 prof->bytes[KFILL_FINALIZE] +=
-                    (run * (2 * near + (D > 0) + (d > 0) + 1) + (tb.W - run) + (s + d + 1 < ch.L ? tb.W : 0)) * 4;
+                    (run * (2 * near + (D > 0) + (d > 0) + 1) + (tb.W - run) + (s + d + 1 < ch.L ? tb.W : 0) +
+                     (fin_h ? (int64_t)tb.W * (2 * near + (D > 0) + 1) : 0)) * 4;
             }
         }
     }

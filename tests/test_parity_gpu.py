@@ -292,9 +292,9 @@ def test_profiling_counts_launches():
 @pytest.mark.parametrize("cfg", [1, 2])
 def test_profiling_device_counts(cfg):
     """Mode 2 runs the counting variants of the fill kernels: the same launches, results and
-    covered counts as mode 1, evaluated counts at most mode 1's (the lower bound only ever
-    skips), the same counts on a second solve (the counters restart with every fill), and
-    the answer the oracle's."""
+    relaxation counts as mode 1, evaluated counts and table bytes at most mode 1's (the
+    lower bound only ever skips), the same product and finalize counts on a second solve
+    (the counters restart with every fill), and the answer the oracle's."""
     ch = make_config_chain(cfg)
     s = rk.Solver(ch)
     try:
@@ -312,14 +312,21 @@ def test_profiling_device_counts(cfg):
         for name in st1:
             n1, _, w1, e1, b1 = st1[name]
             n2, _, w2, e2, b2 = st2[name]
-            assert (n1, w1, b1) == (n2, w2, b2), name
+            assert (n1, w1) == (n2, w2), name
             assert 0 <= e2 <= e1, (name, e1, e2)
-            assert (e2 > 0) == (e1 > 0), name
-            assert st3[name][3] == e2, name
+            assert 0 <= b2 <= b1 and b2 % 4 == 0, (name, b1, b2)
+            assert (e2 > 0) == (e1 > 0) and (b2 > 0) == (b1 > 0), name
+            if name == "k_mid":
+                # a mid tile's skip test reads partials that the launch's other tiles may be
+                # lowering at that moment: its counts may differ from solve to solve
+                assert 0 <= st3[name][3] <= e1 and 0 <= st3[name][4] <= b1, name
+            else:
+                assert st3[name][3:] == st2[name][3:], name
         # from span 64 on, a band product's split ranges pass its 40-split first pass and
         # get cut: fewer candidates than its tiles cover
         if ch.L > 64:
             assert st2["k_product"][3] < st1["k_product"][3]
+            assert st2["k_product"][4] < st1["k_product"][4]
     finally:
         s.close()
 
