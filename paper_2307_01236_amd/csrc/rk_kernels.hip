@@ -443,8 +443,11 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
         }
         const int32_t hi2 = thr == 0xffffffffu ? i_hi : cl - 1;
         if (lo2 <= hi2) {
-            const int32_t gspan = (tau + 2 * SW - 2) / SW * SW;  // rows of a group
-            int32_t anchor = S0 / gspan * gspan + gspan - SW + 1;
+            // the second pass of a group of n2 row blocks starts at the last block's first
+            // split lo2, which lies in every block's uncut range [lo2, i_hi]; a block whose
+            // cut falls below it starts at its own lo2
+            const int32_t n2 = max(1, (tau - PROD_PREFIX - 2) / SW + 2);
+            int32_t anchor = rb / n2 * n2 * SW + (n2 - 1) * SW + 1 + CI * n_pre;
             if (anchor > hi2 || anchor < lo2) anchor = lo2;
             __syncthreads();  // the staging buffer held the thresholds
             pass(lo2, hi2, anchor);
