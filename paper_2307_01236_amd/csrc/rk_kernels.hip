@@ -574,7 +574,22 @@ __device__ __attribute__((always_inline)) inline bool mid_tile(const DevChain &c
     // mids' candidates, which at large spans already make the bound tight: long left spans
     // cost a long recomputation sweep.  (A group B tile folding into the same cells at the
     // same time only lowers the partial; any value it held bounds the final minimum.)
-    if (GA && !LO0) {
+    //
+    // The partials are loaded here and tested after the first split's operand loads have
+    // been issued, so a tile that is not skipped does not wait for the test.
+    constexpr bool TEST = GA && !LO0;
+    int32_t pv[TEST ? R : 1][TEST ? WD : 1];
+    if constexpr (TEST) {
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int32_t s = min(base + r, L - tau - 1);
+            const int32_t *const pr = out + row_of(L, s, s + tau) * stride;
+#pragma unroll
+            for (int k = 0; k < WD; ++k)
+                pv[r][k] = base + r < L - tau && s + tau + k < L ? ldb(pr + (int64_t)k * stride, col) : -DINF;
+        }
+    }
+    auto skip = [&]() {
         int32_t v = -DINF;
 #pragma unroll
         for (int r = 0; r < R; ++r) {
@@ -582,15 +597,14 @@ __device__ __attribute__((always_inline)) inline bool mid_tile(const DevChain &c
             if (s < L - tau) {
                 const int32_t pm = ch.P[(int64_t)s * L + s + lo + 1];
                 const int32_t *const lbr = ch.lb + row_of(L, s, s + tau);
-                const int32_t *const pr = out + row_of(L, s, s + tau) * stride;
 #pragma unroll
                 for (int k = 0; k < WD; ++k)
-                    if (s + tau + k < L) v = max(v, ldb(pr + (int64_t)k * stride, col) - lbr[k] - pm);
+                    if (s + tau + k < L) v = max(v, pv[r][k] - lbr[k] - pm);
             }
         }
         if (m >= W) v = -DINF;
-        if ((int32_t)wave_max_u32((uint32_t)(v + DINF)) <= DINF) return false;
-    }
+        return (int32_t)wave_max_u32((uint32_t)(v + DINF)) <= DINF;
+    };
 
     // the shifts of the tile's splits, read once (a shift x_i > padl happens only when
     // padl >= W: the read lands in the left pad)
@@ -636,6 +650,8 @@ __device__ __attribute__((always_inline)) inline bool mid_tile(const DevChain &c
     auto run = [&](auto dc) {
         constexpr int DL = decltype(dc)::value;
         load(std::integral_constant<int, DL % NS>{}, std::integral_constant<int, 0>{});
+        if constexpr (TEST)
+            if (skip()) return false;
         static_for<0, NS>([&](auto pc) {
             constexpr int p = decltype(pc)::value;
             if constexpr (p + 1 < NS)
@@ -658,19 +674,22 @@ __device__ __attribute__((always_inline)) inline bool mid_tile(const DevChain &c
             }
             __builtin_amdgcn_sched_barrier(0);
         });
+        return true;
     };
     constexpr int G = WD == 16 ? 4 : 2;  // tiles whose split ranges all share a split
     static_assert(R * (G - 1) < NS, "a group's ranges overlap");
     const int32_t wg = g % G;
+    bool ran;
     if constexpr (G == 4) {
-        if (wg == 0) run(std::integral_constant<int, 3 * R>{});
-        else if (wg == 1) run(std::integral_constant<int, 2 * R>{});
-        else if (wg == 2) run(std::integral_constant<int, R>{});
-        else run(std::integral_constant<int, 0>{});
+        if (wg == 0) ran = run(std::integral_constant<int, 3 * R>{});
+        else if (wg == 1) ran = run(std::integral_constant<int, 2 * R>{});
+        else if (wg == 2) ran = run(std::integral_constant<int, R>{});
+        else ran = run(std::integral_constant<int, 0>{});
     } else {
-        if (wg == 0) run(std::integral_constant<int, R>{});
-        else run(std::integral_constant<int, 0>{});
+        if (wg == 0) ran = run(std::integral_constant<int, R>{});
+        else ran = run(std::integral_constant<int, 0>{});
     }
+    if (!ran) return false;
 
     // store (or fold into the stored partial) through one descriptor per row r: group A
     // cell (s0+r, s0+r+tau+k) is k rows after (s0+r, s0+r+tau); group B cell
