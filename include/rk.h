@@ -162,7 +162,7 @@ int rk_solve_async(rk_chain *c, int32_t M, void *d_workspace, size_t ws_bytes, v
  *     rk_solve_async, which upload its derived arrays), with the same option-pruning
  *     setting, and profiling must be off; else RK_E_INVAL.
  *   - RK_E_NOMEM when rk_workspace_bytes(c, M) exceeds RK_NOALLOC_MAX_BYTES (about
- *     L = 64 blocks at M = 3500, or L = 128 at M = 895, with activations of at most
+ *     L = 64 blocks at M = 2500, or L = 128 at M = 575, with activations of at most
  *     64 slots).
  *   - Every call on a device shares that device's array and overwrites what the previous
  *     call left there: reads of an earlier call's results are valid only until the next

@@ -106,8 +106,8 @@ int geometry(const rk_chain *c, int32_t M, Geometry *g, size_t *bytes)
     g->padl = rk::round64(std::min<int64_t>(c->h.max_x, g->W));
     g->stride = g->padl + rk::round64(g->W);
     g->rows = rk::n_rows(c->h.L) + 1;
-    // Opt and ap; with the saving sweep also H and aq
-    const int64_t elems = (c->h.refwd.empty() ? 2 : 4) * rk::table_rows(c->h.L) * (int64_t)g->stride;
+    // Opt, ap and the right operand table; with the saving sweep also H and aq
+    const int64_t elems = (c->h.refwd.empty() ? 3 : 5) * rk::table_rows(c->h.L) * (int64_t)g->stride;
     if (elems <= 0 || elems > (int64_t(1) << 40)) return RK_E_NOMEM;
     // the products address each operand block with 32-bit byte offsets from its first row;
     // the widest block spans OFFSET_SPAN_L (L - 1) + OFFSET_SPAN_C rows
@@ -226,8 +226,9 @@ int fill(rk_chain *c, int32_t M, const Geometry &g, int32_t *tables, hipStream_t
     const int64_t tsz = rk::table_rows(c->h.L) * (int64_t)g.stride;
     c->tb.opt = tables + rk::SLACK * (int64_t)g.stride;
     c->tb.ap = c->tb.opt + tsz;
-    c->tb.hopt = c->dc.c3 ? c->tb.ap + tsz : nullptr;
-    c->tb.aq = c->dc.c3 ? c->tb.ap + 2 * tsz : nullptr;
+    c->tb.os = c->tb.ap + tsz;
+    c->tb.hopt = c->dc.c3 ? c->tb.os + tsz : nullptr;
+    c->tb.aq = c->dc.c3 ? c->tb.os + 2 * tsz : nullptr;
     // profiled fills launch their kernels one by one, never inside a graph: with counting on,
     // the counting variants of the kernels add what only they know (evaluated and skipped
     // candidates) into a small device array

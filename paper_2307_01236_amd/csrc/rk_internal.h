@@ -12,9 +12,15 @@
 // starts 256-byte aligned.
 //
 //   opt  Opt(s,t,m) at opt[row(s,t)*stride + padl + m].  The left pad lets a
-//        read at m - x_i (Eq. fn's right subproblem) run unmasked: columns
-//        below 0 read infinity.  Before a span is final its slot holds the
-//        partial minimum that the band products left there.
+//        read at m - xbar (case 1) run unmasked: columns below 0 read
+//        infinity.  Before a span is final its slot holds the partial minimum
+//        that the products left there.
+//   os   the right operand of Eq. fn, written with Opt when a row becomes final:
+//        os[row(i,t)*stride + padl + m] = Opt(i,t,m - x_i) for x_i <= m < W,
+//        infinity below x_i, so a split's right operand is read at column m,
+//        in step with its left operand and 256-byte aligned like it (read at
+//        m - x_i in opt, a wave's 256 bytes straddle three 128-byte lines
+//        unless x_i is a multiple of 32).
 //   ap   the left operand of Eq. fn, precomputed when a row becomes final:
 //        ap[row(s,i-1)*stride + padl + m] = P[s][i] + Opt(s,i-1,m) if the
 //        no-save sweep s..i-1 fits in m, else infinity (saturated).
@@ -94,6 +100,7 @@ constexpr int32_t HMAX = 256;
 struct Tables {
     int32_t *opt;
     int32_t *ap;
+    int32_t *os;  // the right operand table (above)
     // with the saving sweep (else null): H(s,t,u) and its left operand
     // aq[row(s,i-1)*stride + padl + v] = P[s][i] + Opt(s,i-1,v) if the sweep s..i-1 with its
     // input fits v + x_s, else infinity (H reads it at v = u - x_s)

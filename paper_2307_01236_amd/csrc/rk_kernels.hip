@@ -87,7 +87,7 @@ __global__ __launch_bounds__(256) void k_init_inf_rows(Tables tb)
     const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
     const int32_t y = (int32_t)blockIdx.y, k = y % PER_TABLE, table = y / PER_TABLE;
     const int64_t row = k < SLACK ? (int64_t)k - SLACK : tb.inf_row + (k - SLACK);
-    int32_t *const base = table == 0 ? tb.opt : table == 1 ? tb.ap : table == 2 ? tb.hopt : tb.aq;
+    int32_t *const base = table == 0 ? tb.opt : table == 1 ? tb.ap : table == 2 ? tb.os : table == 3 ? tb.hopt : tb.aq;
     if (j < tb.stride) base[row * tb.stride + j] = DINF;
     if (tb.ctr && blockIdx.x == 0 && y == 0)
         for (int32_t k = (int32_t)threadIdx.x; k < CTR_SLOTS; k += 256) tb.ctr[k * CTR_PITCH] = 0;
@@ -228,7 +228,7 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
     const uint32_t m = mchunk * 64 + lane;
     const uint32_t colb = (uint32_t)(padl + min(m, (uint32_t)tb.W - 1)) * 4u;
     const uint32_t pitch = (uint32_t)stride * 4u;
-    const int32_t *const opt_end = tb.opt + (tb.inf_row + 1 + SLACK) * stride;
+    const int32_t *const os_end = tb.os + (tb.inf_row + 1 + SLACK) * stride;
     const int32_t *const ap_end = left + (tb.inf_row + 1 + SLACK) * stride;
     const int32_t t0 = S0 + tau;  // first end the workgroup covers
     const int32_t i_lo = S0 + 1, i_hi = min(S0 + SW - 1 + tau, L - 1);
@@ -265,14 +265,14 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
     // where the chunk order wraps around.
     const int32_t *qcur = nullptr, *acur = nullptr;
     auto seek = [&](int32_t ic) {
-        qcur = tb.opt + (row_of(L, ic, t0) - 1) * stride;
+        qcur = tb.os + (row_of(L, ic, t0) - 1) * stride;
         acur = left + row_of(L, s0, ic - 1) * stride;
     };
     auto fetch = [&](int32_t ic) {
-        // right operands from one row before (ic, t0): split i's rows start rel(i) rows on,
-        // shifted left by min(x_i, padl) columns (a larger x_i reads only the left pad)
+        // right operands from one row before (ic, t0): split i's rows start rel(i) rows on
+        // (the right operand table holds Opt(i, t, m - x_i) at column m)
         const int32_t *const qb = qcur;
-        const __amdgpu_buffer_rsrc_t rq = block_rsrc(qb, opt_end);
+        const __amdgpu_buffer_rsrc_t rq = block_rsrc(qb, os_end);
         // Operands that are not used are not read: a staged row whose right span
         // t0 + jj*NW + wave - ic - ii is outside [0, tau), or a left operand whose span
         // ic + ii - 1 - s0 - r is, loads from OOB (value 0; a candidate it takes part in has
@@ -283,8 +283,7 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
 #pragma unroll
         for (int ii = 0; ii < CI; ++ii) {
             const int32_t i = ic + ii;
-            const uint32_t xs = (uint32_t)min(ch.x[min(i, L)], padl);
-            const uint32_t so = rel * pitch - 4u * xs;
+            const uint32_t so = rel * pitch;
             if (qall) {
 #pragma unroll
                 for (int jj = 0; jj < JW; ++jj) qv[ii][jj] = buf_load(rq, qoff[jj], so);
@@ -524,9 +523,10 @@ __device__ __attribute__((always_inline)) inline bool mid_tile(const DevChain &c
     const int32_t padl = tb.padl;
     const int32_t m = mc * 64 + lane;
     const uint32_t col = (uint32_t)(padl + min(m, W - 1)) * 4u;
-    const int32_t *const opt_end = tb.opt + (tb.inf_row + 1 + SLACK) * stride;
+    const int32_t *const os_end = tb.os + (tb.inf_row + 1 + SLACK) * stride;
     // case 2 of Opt (left ap, into opt) or, with hp, H of the saving sweep (left aq read x_s
-    // columns to the left, into hopt)
+    // columns to the left, into hopt); the right operand Opt(i, t, m - x_i) from the right
+    // operand table at column m
     const int32_t *const left = hp ? tb.aq : tb.ap;
     int32_t *const out = hp ? tb.hopt : tb.opt;
     const int32_t *const ap_end = left + (tb.inf_row + 1 + SLACK) * stride;
@@ -606,12 +606,6 @@ __device__ __attribute__((always_inline)) inline bool mid_tile(const DevChain &c
         return (int32_t)wave_max_u32((uint32_t)(v + DINF)) <= DINF;
     };
 
-    // the shifts of the tile's splits, read once (a shift x_i > padl happens only when
-    // padl >= W: the read lands in the left pad)
-    int32_t xsh[NS];
-#pragma unroll
-    for (int u = 0; u < NS; ++u) xsh[u] = min(ch.x[min(i0 + u, L - 1)], padl);
-
     uint32_t vr[2][R], vj[2][NJ];
     // Split u (i = i0 + u) is real for operand r in [u - WD + 1, u]; operand j is needed in
     // [rlo, rhi + WD - 1].  Splits past L - 1 only serve cells past the table (clamped).
@@ -620,8 +614,7 @@ __device__ __attribute__((always_inline)) inline bool mid_tile(const DevChain &c
         constexpr int rlo = u - WD + 1 > 0 ? u - WD + 1 : 0, rhi = u < R - 1 ? u : R - 1;
         constexpr int jhi = LO0 ? (rhi + WD - 1 < u ? rhi + WD - 1 : u) : rhi + WD - 1;
         const int32_t i = min(i0 + u, L - 1);
-        const int32_t xs = xsh[u];
-        const __amdgpu_buffer_rsrc_t dq = block_rsrc(tb.opt + row_of(L, i, base + tau) * stride - xs, opt_end);
+        const __amdgpu_buffer_rsrc_t dq = block_rsrc(tb.os + row_of(L, i, base + tau) * stride, os_end);
         const __amdgpu_buffer_rsrc_t da = block_rsrc(left + row_of(L, sa, i0 + u - 1) * stride, ap_end);
 #pragma unroll
         for (int r = rlo; r <= rhi; ++r) vr[b][r] = buf_load(GA ? da : dq, roff[r], 0);
@@ -812,24 +805,23 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
     for (int c = 0; c < NC; ++c) col[c] = (uint32_t)min(ml + 64 * c, W - 1) * 4u;
 
     // splits i0 .. i0+n-1: left(s, i-1) + Opt(i, t, m - x_i), left = ap (Opt) or aq read lsh
-    // columns to the left (H).  Pointers at column 0: row (s, i-1) is i-1-s rows after
-    // (s, s); Opt row (i+1, t) is L-1-i rows after (i, t)
+    // columns to the left (H), the right operand from the right operand table at column m.
+    // Pointers at column 0: row (s, i-1) is i-1-s rows after (s, s); row (i+1, t) is L-1-i
+    // rows after (i, t)
     int32_t best[NC];
     auto splits = [&](const int32_t *ltab, int32_t lsh, int32_t i0, int32_t n) {
         const int32_t *pa = ltab + (row_of(L, s, s) + (i0 - 1 - s)) * stride + padl - lsh;
-        const int32_t *pq = tb.opt + row_of(L, i0, t) * stride + padl;
+        const int32_t *pq = tb.os + row_of(L, i0, t) * stride + padl;
         int32_t i = i0;
         for (int32_t j0 = 0; j0 < n; j0 += FB) {
             int32_t va[FB][NC], vq[FB][NC];
 #pragma unroll
             for (int u = 0; u < FB; ++u) {
                 if (j0 + u < n) {
-                    // a shift x_i > padl happens only when padl >= W: the read lands in the left pad
-                    const int32_t *const q = pq - min(ch.x[i], padl);
 #pragma unroll
                     for (int c = 0; c < NC; ++c) {
                         va[u][c] = ldrow(pa, pitch, col[c]);
-                        vq[u][c] = ldrow(q, pitch, col[c]);
+                        vq[u][c] = ldrow(pq, pitch, col[c]);
                     }
                     pa += stride;
                     pq += (int64_t)(L - 1 - i) * stride;
@@ -973,8 +965,10 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
         }
         return;
     }
-    // Opt, the left operand ap(s, t+1) of Eq. fn and, with the saving sweep, the left operand
-    // aq(s, t+1, v) = P[s][t+1] + Opt(s, t, v) of H(s, .) if the sweep s..t fits v + x_s
+    // Opt, its copy in the right operand table (Opt(s, t, m) at column m + x_s, infinity
+    // below x_s), the left operand ap(s, t+1) of Eq. fn and, with the saving sweep, the left
+    // operand aq(s, t+1, v) = P[s][t+1] + Opt(s, t, v) of H(s, .) if the sweep s..t fits v + x_s
+    int32_t *const srow = tb.os + row_st * stride + padl;
     int32_t *const arow = tb.ap + row_st * stride + padl;
     int32_t *const qrow = tb.aq ? tb.aq + row_st * stride + padl : nullptr;
     const int32_t need2 = t + 1 < L ? ch.need2[ip] : 0, P = t + 1 < L ? ch.P[ip] : 0;
@@ -989,6 +983,8 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
         if (m < W) {
             const int32_t v = min(best[c], DINF);
             orow[m] = v;
+            if (m < xs) srow[m] = DINF;
+            if ((int64_t)m + xs < W) srow[m + xs] = v;
             if (t + 1 < L) {
                 arow[m] = m >= need2 ? min(P + v, DINF) : DINF;
                 if (qrow) qrow[m] = m + xs >= need3 ? min(P + v, DINF) : DINF;
@@ -1156,7 +1152,7 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
     hipError_t e;
     int32_t n = 0;
     const int32_t midmin = fill_midmin(ch.L, tb.W);
-    e = launch(prof, KFILL_INIT, k_init_inf_rows, dim3((tb.stride + 255) / 256, (tb.hopt ? 4 : 2) * (2 * SLACK + 1)),
+    e = launch(prof, KFILL_INIT, k_init_inf_rows, dim3((tb.stride + 255) / 256, (tb.hopt ? 5 : 3) * (2 * SLACK + 1)),
                dim3(256), stream, tb);
     if (e != hipSuccess) return e;
     ++n;
@@ -1223,7 +1219,8 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
         if (prof->on) {
             // per cell, in the workgroups below msa: two operand rows per split, the stored
             // partial, the case-1 row, the Opt row written; past msa only the Opt row
-            // written; the ap row written where a later split uses it.  With the saving
+            // written; and everywhere the right operand row written, and the ap row (with the
+            // saving sweep also the aq row) where a later split uses it.  With the saving
             // sweep, H's workgroups (every column, d >= 1): two operand rows per split, the
             // stored partial and the H row written.
             for (int32_t s = 0; s + d < ch.L; ++s) {
@@ -1231,7 +1228,8 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
                 prof->eval[KFILL_FINALIZE] += run * (near + ch.K + (tb.hopt && d >= 2 ? ch.K : 0)) +
                                               (tb.hopt ? (int64_t)tb.W * near : 0);
                 prof->bytes[KFILL_FINALIZE] +=
-                    (run * (2 * near + (D > 0) + (d > 0) + 1) + (tb.W - run) + (s + d + 1 < ch.L ? tb.W : 0) +
+                    (run * (2 * near + (D > 0) + (d > 0) + 1) + (tb.W - run) + tb.W +
+                     (s + d + 1 < ch.L ? (int64_t)tb.W * (tb.aq ? 2 : 1) : 0) +
                      (fin_h ? (int64_t)tb.W * (2 * near + (D > 0) + 1) : 0)) * 4;
             }
         }

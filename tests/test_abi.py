@@ -127,7 +127,7 @@ def test_workspace_guard_for_32bit_offsets():
             return (64 + (M + 1 + 63) // 64 * 64) * 4
         span = 18 * ch.L + 64
         ok = max(M for M in range(70_000, 80_000, 64) if span * row_bytes(M) < 2 ** 31)
-        assert rk.rk_workspace_bytes(h, ok) > 0  # ~60 GB of tables: accepted
+        assert rk.rk_workspace_bytes(h, ok) > 0  # ~90 GB of tables: accepted
         with pytest.raises(rk.RKError) as e:
             rk.rk_workspace_bytes(h, ok + 64)
         assert e.value.code == rk.RK_E_NOMEM
@@ -143,12 +143,12 @@ def test_workspace_bytes():
     ch = make_config_chain(4)
     h = rk.rk_chain_create(*_args(ch))
     try:
-        # two tables (Opt and the case-2 left operand), each with one extra all-infinity row
-        # and 32 rows of slack at either end; rows are a 64-column infinity pad (max x_i = 7
-        # here) plus the budget columns
+        # three tables (Opt, the case-2 left operand and its right operand laid out at column
+        # m), each with one extra all-infinity row and 32 rows of slack at either end; rows are
+        # a 64-column infinity pad (max x_i = 7 here) plus the budget columns
         rows = ch.L * (ch.L + 1) // 2 + 1 + 64
-        assert rk.rk_workspace_bytes(h, 6000) == 2 * rows * (64 + 6016) * 4
-        assert rk.rk_workspace_bytes(h, 0) == 2 * rows * (64 + 64) * 4
+        assert rk.rk_workspace_bytes(h, 6000) == 3 * rows * (64 + 6016) * 4
+        assert rk.rk_workspace_bytes(h, 0) == 3 * rows * (64 + 64) * 4
         with pytest.raises(rk.RKError):
             rk.rk_workspace_bytes(h, -1)
         with pytest.raises(rk.RKError):
@@ -193,7 +193,7 @@ def test_saving_sweep_arguments():
         assert rk.rk_workspace_bytes(h, 100) == W0  # unchanged after the refusals
         ok = np.ones((ch.L, ch.K), dtype=np.int32)
         rk.rk_chain_set_saving_sweep(h, ok)
-        assert rk.rk_workspace_bytes(h, 100) == 2 * W0
+        assert 3 * rk.rk_workspace_bytes(h, 100) == 5 * W0  # two more tables of the same shape
         rk.rk_chain_set_saving_sweep(h, None)
         assert rk.rk_workspace_bytes(h, 100) == W0
         assert lib.rk_chain_set_saving_sweep(None, None) == rk.RK_E_INVAL
