@@ -353,6 +353,21 @@ def main():
     fill_s = statistics.median(fill_ms) * 1e-3
     evaluated = sum(v[3] for v in kern.values()) / args.steps
     table_bytes = sum(v[4] for v in kern.values()) / args.steps
+    # every fill kernel against both roofs (per launch, from the same profiled steps), with
+    # its measured HBM traffic per launch where the committed counter summary is current
+    roofline["per_kernel"] = {}
+    for name, (n, ms, _, work, moved) in kern.items():
+        if n == 0 or ms <= 0 or work == 0:
+            continue
+        t_s = ms / n * 1e-3
+        meas, _ = measured_traffic(ch.name, name)
+        roofline["per_kernel"][name] = {
+            "launches_per_step": n / args.steps, "avg_launch_ms": ms / n,
+            "valu_frac": OPS_PER_RELAX * work / n / t_s / 1e12 / VALU_PEAK_TOPS,
+            "hbm_frac_compulsory": moved / n / t_s / 1e9 / HBM_PEAK_GBS,
+            "measured_bytes_per_launch": meas,
+            "hbm_frac_measured": meas / t_s / 1e9 / HBM_PEAK_GBS if meas is not None else None,
+        }
     roofline["whole_fill"] = {
         "fill_ms": fill_s * 1e3, "launches": sum(v[0] for v in kern.values()) / args.steps,
         "relaxations_nominal": relax, "relaxations_evaluated": evaluated,
