@@ -456,13 +456,20 @@ __global__ __launch_bounds__(NW * 64) void k_product(DevChain ch, Tables tb, int
     if (CNT && threadIdx.x == 0)  // profiling: every cell of the tile relaxed its splits i <= e_last
         tb.rec[(int64_t)(hp ? n_chunks + chunk : chunk) * n_rb + rb] = e_last + 1;
     if (m >= (uint32_t)tb.W) return;
+    // the wave's ends t0r..t0r+TW-1 of row s are consecutive rows: one descriptor per row s
+    // covers those inside the table, and a store past them is dropped by its range check
+    const uint32_t cst = (uint32_t)(padl + m) * 4u;
 #pragma unroll
-    for (int r = 0; r < SR; ++r)
+    for (int r = 0; r < SR; ++r) {
+        const int32_t s = s0 + r, t0r = s + tau + kh;
+        if (s >= s_end || t0r >= L) continue;
+        const int32_t nk = min(TW, L - t0r);
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            out + row_of(L, s, t0r) * stride, (short)0, (int)(nk * pitch), 0x00020000);
 #pragma unroll
-        for (int k = 0; k < TW; ++k) {
-            const int32_t s = s0 + r, t = s + tau + kh + k;
-            if (s < s_end && t < L) out[row_of(L, s, t) * stride + padl + m] = (int32_t)acc[r][k];
-        }
+        for (int k = 0; k < TW; ++k)
+            __builtin_amdgcn_raw_buffer_store_b32((int32_t)acc[r][k], rs, (int)(cst + (uint32_t)k * pitch), 0, 0);
+    }
 }
 
 // ---------------------------------------------------------------------------------------
