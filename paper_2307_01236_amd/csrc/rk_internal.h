@@ -49,14 +49,13 @@ static_assert(RK_TIME_LIMIT < DINF, "finite values must stay below the device in
 
 // Spans per band: every band of BAND span lengths gets one tiled product over
 // the splits whose two operands are older than the band.  Inside a band, mid
-// products every midmin spans cover the splits whose longer operand lies in the
-// band's earlier part, so that a diagonal's own launch adds fewer than 2 midmin.
-// midmin is 4 for tables of at least MID4_MIN_LW (blocks x budget columns), where
-// the narrowest mid level saves the finalize more table reads than its own launches
-// cost, and 8 below.
+// products every MIDMIN spans cover the splits whose longer operand lies in the
+// band's earlier part, so that a diagonal's own launch adds fewer than 2 MIDMIN.
+// (A level of width 4 saved the finalize more table reads than its 48 launches
+// cost only while the finalize read its right operands unaligned and without the
+// lower bound; now it costs 0.3 ms on every table size measured.)
 constexpr int32_t BAND = 32;
-constexpr int64_t MID4_MIN_LW = 1600000;
-inline int32_t fill_midmin(int32_t L, int32_t W) { return (int64_t)L * W >= MID4_MIN_LW ? 4 : 8; }
+constexpr int32_t MIDMIN = 8;
 
 // Splits per chunk of the band product.
 constexpr int32_t PROD_CI = 2;

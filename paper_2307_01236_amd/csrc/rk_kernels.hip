@@ -1158,7 +1158,7 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
     static_assert(BAND == 32, "the launch sequence below is written for 32-span bands");
     hipError_t e;
     int32_t n = 0;
-    const int32_t midmin = fill_midmin(ch.L, tb.W);
+    const int32_t midmin = MIDMIN;
     e = launch(prof, KFILL_INIT, k_init_inf_rows, dim3((tb.stride + 255) / 256, (tb.hopt ? 5 : 3) * (2 * SLACK + 1)),
                dim3(256), stream, tb);
     if (e != hipSuccess) return e;
@@ -1207,8 +1207,6 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
             if ((e = launch_mid<16>(ch, tb, stream, d, &n, prof)) != hipSuccess) return e;
         } else if (d % 8 == 0 && d > 0) {
             if ((e = launch_mid<8>(ch, tb, stream, d, &n, prof)) != hipSuccess) return e;
-        } else if (d % 4 == 0 && d > 0 && midmin == 4) {
-            if ((e = launch_mid<4>(ch, tb, stream, d, &n, prof)) != hipSuccess) return e;
         }
         int32_t sat = 0;  // chunks from n_run on lie past every cell's msa: they only store
         for (int32_t s = 0; s + d < ch.L; ++s) sat = max(sat, ch.h_msa[row_of(ch.L, s, s + d)]);

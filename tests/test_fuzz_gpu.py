@@ -4,10 +4,11 @@ Three kinds of chains, every one compared in full (Opt table, choice table, answ
 schedule), with option pruning alternating:
 - small: 1-89 blocks, 1-39 options, sizes and times that may be zero, a quarter with
   identical blocks, a few time values only (ties), budgets from 0 to a bit above storing
-  everything; every fourth chain is short with a budget near 1.6e6 / L columns, on either
-  side of the threshold of the width-4 mid level;
-- big: 90-199 blocks with budgets below 350 (several bands, every mid width but 4);
-- big4: 64-109 blocks with tables past that threshold (several bands and the width-4 level).
+  everything; every fourth chain is short with a budget near 1.6e6 / L columns (thousands
+  of column chunks, large left pads);
+- big: 90-199 blocks with budgets below 350 (several bands, both mid widths);
+- big4: 64-109 blocks with tables of at least 1.6e6 blocks x budget columns (several bands,
+  both mid widths, a few hundred column chunks).
 """
 import numpy as np
 import pytest

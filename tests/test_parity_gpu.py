@@ -568,10 +568,10 @@ def test_medium_random_chains_sampled(idx):
 
 
 @pytest.mark.parametrize("M", [24998, 25000])
-def test_mid_width_four_on_and_off(M):
-    """64 blocks at budgets either side of the table size (blocks x budget columns =
-    1.6e6) from which the fill adds mid products of width 4 and its finalize covers only the
-    splits whose longer operand spans the last 4 spans: full-table parity in both regimes."""
+def test_mid_levels_at_large_budgets(M):
+    """64 blocks at about 25 000 budget columns (1.6e6 blocks x budget columns) with shifts of
+    up to 50 columns: mid products of widths 16 and 8 and a finalize that covers the splits
+    whose longer operand spans the last 8 spans.  Full-table parity."""
     ch = make_random_chain(6464, 64, 3, xmax=50, amax=400, tmax=100, tmin=0)
     sol = full_parity(ch, M)
     assert sol.answer != INF
@@ -585,15 +585,14 @@ def test_mid_width_four_on_and_off(M):
         assert sum(v[2] for v in stats.values()) == relaxations(ch.L, ch.K, M)
     finally:
         s.close()
-    # mids of width 16 at d = 16, 48 and of width 8 at d = 8, 24, 40, 56; of width 4 at
-    # d = 4, 12, ..., 60 when blocks x budget columns reaches 1.6e6
-    assert n_mid == (14 if ch.L * (M + 1) >= 1_600_000 else 6), n_mid
+    # mids of width 16 at d = 16, 48 and of width 8 at d = 8, 24, 40, 56
+    assert n_mid == 6, n_mid
 
 
 @pytest.mark.parametrize("seed", [97003, 97008])
-def test_several_bands_with_width_four_mids(seed):
-    """Chains of 64-110 blocks whose tables pass 1.6e6 blocks x budget columns (78 and 105
-    blocks, one option): two or three band products, mids of widths 16, 8 and 4, and shifts
+def test_several_bands_at_large_tables(seed):
+    """Chains of 64-110 blocks with at least 1.6e6 blocks x budget columns (78 and 105
+    blocks, one option): two or three band products, mids of widths 16 and 8, and shifts
     of up to a few hundred columns.  Full-table parity."""
     rng = np.random.default_rng(seed)
     L = int(rng.integers(64, 110))

@@ -56,9 +56,9 @@ def test_multi_band_chains_with_sweep(seed):
     full_parity(ch, min(store_all_bound(ch) // 3, 400), prune=seed == 0)
 
 
-def test_width4_chain_with_sweep():
-    """64 blocks x 25 001 budget columns, past 1.6e6: mid products of width 4 run for H too,
-    and the finalize covers only the splits whose longer operand spans the last 4 spans."""
+def test_large_table_with_sweep():
+    """64 blocks x 25 001 budget columns: the mid products of widths 16 and 8 run for H too,
+    and the finalize covers the splits whose longer operand spans the last 8 spans."""
     ch = make_random_chain(6464, 64, 3, xmax=50, amax=400, tmax=100, tmin=0)
     full_parity(with_refwd(ch, 3, 0.0, 0.5), 25000)
 
