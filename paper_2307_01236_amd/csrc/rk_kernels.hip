@@ -141,9 +141,9 @@ static inline uint32_t chunk_grid(int32_t n_chunks, int32_t n_idx)
 // groups of SR rows; each row group's T ends are split over TH waves, so a wave keeps, per
 // lane, the SR x TW accumulators of rows s0..s0+SR-1 and ends t = s + tau + kh + k (TW = T/TH
 // ends from kh on).  Splits are taken CI at a time.  The right operands
-// Opt(i, t, .) of a chunk, for all NQ ends of the workgroup, are staged in LDS (each
-// global row read once, then used by up to SR waves x rows); each wave reads its own left
-// operands ap(s, i).  The next chunk's operands are loaded into registers while the
+// Opt(i, t, m - x_i) of a chunk, for all NQ ends of the workgroup, are read from the right
+// operand table at column m and staged in LDS (each global row read once, then used by up
+// to SR waves x rows); each wave reads its own left operands ap(s, i).  The next chunk's operands are loaded into registers while the
 // current one is relaxed.
 //
 // Which candidates are real: split i of cell (s,t) needs s < i <= t and both operand
