@@ -131,6 +131,7 @@ int ensure_device(rk_chain *c)
         c->queued = false;
         c->bt_fill = -1;
     }
+    if (!c->h.refwd.empty() && c->h.msaH.size() != c->h.msa.size()) return RK_E_INTERNAL;  // sizes H's launches
     rk::host_run_slots(c->h, c->prune, c->run);
     c->run_prune = c->prune;
     c->run_version = c->host_version;
@@ -161,6 +162,7 @@ int ensure_device(rk_chain *c)
     c->dc.c3 = sweep ? put(c->run.c3) : nullptr;
     c->dc.need3 = sweep ? put(c->h.need3) : nullptr;
     c->dc.h_msa = c->h.msa.data();
+    c->dc.h_msaH = sweep ? c->h.msaH.data() : nullptr;
     int64_t xbar_max = 0;
     for (int32_t v : c->run.xbar) xbar_max = std::max<int64_t>(xbar_max, v);
     c->dc.xbar_halo = xbar_max > rk::HMAX ? rk::HMAX + 1 : rk::round64(xbar_max);
@@ -335,7 +337,13 @@ int rk_chain_set_saving_sweep(rk_chain *c, const int32_t *refwd)
     try {
         rk::HostChain h = c->h;  // left unchanged on an error
         rc = rk::host_set_refwd(h, refwd);
-        if (rc == RK_OK) c->h.refwd.swap(h.refwd), c->h.c3.swap(h.c3), c->h.need3.swap(h.need3), c->h.kept.swap(h.kept);
+        if (rc == RK_OK) {
+            c->h.refwd.swap(h.refwd);
+            c->h.c3.swap(h.c3);
+            c->h.need3.swap(h.need3);
+            c->h.msaH.swap(h.msaH);
+            c->h.kept.swap(h.kept);
+        }
     } catch (...) {
         rc = RK_E_NOMEM;
     }

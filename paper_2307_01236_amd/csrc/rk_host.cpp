@@ -160,6 +160,7 @@ int host_set_refwd(HostChain &h, const int32_t *refwd)
         h.refwd.clear();
         h.c3.clear();
         h.need3.clear();
+        h.msaH.clear();
         prune(h);
         return RK_OK;
     }
@@ -182,6 +183,14 @@ int host_set_refwd(HostChain &h, const int32_t *refwd)
             h.need3[(size_t)s * L + i] = (int32_t)std::min(need, kSizeCap);
         }
     }
+    h.msaH.assign(h.msa.size(), (int32_t)kSizeCap);
+    for (int32_t s = 0; s + 1 < L; ++s)
+        for (int32_t t = s + 1; t < L; ++t) {
+            const int64_t v = std::max<int64_t>({h.need3[(size_t)s * L + s + 1],
+                                                 (int64_t)h.msa[(size_t)row(L, s, s)] + h.x[s],
+                                                 (int64_t)h.msa[(size_t)row(L, s + 1, t)] + h.x[s + 1]});
+            h.msaH[(size_t)row(L, s, t)] = (int32_t)std::min(v, kSizeCap);
+        }
     prune(h);
     return RK_OK;
 }

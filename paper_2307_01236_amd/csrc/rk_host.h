@@ -23,6 +23,11 @@ struct HostChain {
     // The saving sweep (empty when off): refwd, c3 = r(F)+r(B)+refwd [L*K]; need3[s*L+i] =
     // max_{k=s}^{i-1} x_k + x_{k+1} + tmp(F_k^0), the sweep of H(s, .) that drops its input
     std::vector<int32_t> refwd, c3, need3;
+    // From budget msaH(s,t) on (t > s), H(s,t,u) = lb(s,t) + P[s][s+1]: every candidate of H
+    // is at least lb(s,t) + P[s][i] >= lb(s,t) + P[s][s+1], and split s+1 reaches it once its
+    // sweep fits (need3[s][s+1] <= u) and both of its parts are past their msa
+    // (u - x_s >= msa(s,s), u - x_{s+1} >= msa(s+1,t)); [L(L+1)/2] like msa
+    std::vector<int32_t> msaH;
     std::vector<uint8_t> kept;  // [L*K] option survives the dominance test
     int32_t max_x = 0;          // largest x_i over the split points i = 1..L-1
 };

@@ -90,6 +90,7 @@ struct DevChain {
     // [L*K], need3 [L*L] the thresholds of the sweeps of H (the input inside the budget).
     const int32_t *c3;
     const int32_t *need3;
+    const int32_t *h_msaH;  // [L(L+1)/2], host memory: from msaH(s,t) on, H(s,t) = lb(s,t) + P[s][s+1]
     int32_t xbar_halo;     // round64(max xbar): how far left case 1 reads from column m
 };
 

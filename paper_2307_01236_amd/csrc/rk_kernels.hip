@@ -778,7 +778,8 @@ __device__ inline int32_t ldrow(const int32_t *base, uint32_t pitch, uint32_t by
 
 template <bool CNT>
 __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t d, int32_t midmin,
-                                                 int32_t n_chunks, int32_t n_run, int32_t n_chunks_h)
+                                                 int32_t n_chunks, int32_t n_run, int32_t n_chunks_h,
+                                                 int32_t n_run_h)
 {
     constexpr int32_t FB = 8, NC = FC / FT, NST = (HMAX + FC) / FT;
     __shared__ int32_t seg[HMAX + FC], seg3[HMAX + FC];
@@ -869,7 +870,13 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
     // store.  The products and mids of these spans ran on at least the chunks below n_run.
     // (The stores stay after every load on every path, so the loads of the per-block and
     // per-option arrays may use the scalar cache.)
-    if (hp) {
+    if (hp && chunk >= n_run_h) {
+        // past msaH(s,t) of every cell of the diagonal: H(s,t) = lb(s,t) + P[s][s+1] (the
+        // lower bound of every candidate, reached by split s+1); the products did not run here
+        const int32_t hv = ch.lb[row_st] + ch.P[(int64_t)s * L + s + 1];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) best[c] = hv;
+    } else if (hp) {
         // H(s, t) = min_i aq(s, i, m - x_s) + Opt(i, t, m - x_i): the products' partial, then
         // the near splits
         const int32_t *const hrow = tb.hopt + row_st * stride + padl;
@@ -1102,7 +1109,12 @@ static hipError_t launch_mid(const DevChain &ch, const Tables &tb, hipStream_t s
     int32_t sat = 0;
     for (int32_t s = 0; s < L - d; ++s) sat = max(sat, ch.h_msa[row_of(L, s, min(s + d + WD - 1, L - 1))]);
     const int32_t n_chunks = min(n_mc, run_chunks(sat));
-    const int32_t n_chunks_h = tb.hopt ? n_mc : 0;  // H of the saving sweep: every chunk
+    int32_t n_chunks_h = 0;  // H of the saving sweep: the chunks below the largest msaH
+    if (tb.hopt) {
+        int32_t sat_h = 0;
+        for (int32_t s = 0; s < L - d; ++s) sat_h = max(sat_h, ch.h_msaH[row_of(L, s, min(s + d + WD - 1, L - 1))]);
+        n_chunks_h = min(n_mc, run_chunks(sat_h));
+    }
     const int64_t w1 = lo == 0 ? product_work(L, tb.W, d, WD, 0, WD, 0, WD)
                                : product_work(L, tb.W, d, WD, lo, d, 0, d) + product_work(L, tb.W, d, WD, 0, lo, lo, d);
     prof->work[KFILL_MID] += w1 * (tb.hopt ? 2 : 1);
@@ -1171,7 +1183,13 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
             for (int32_t s = 0; s < ch.L - d; ++s)
                 sat = max(sat, ch.h_msa[row_of(ch.L, s, min(s + d + BAND - 1, ch.L - 1))]);
             const int32_t n_chunks = min((tb.W + 63) / 64, run_chunks(sat));
-            const int32_t n_chunks_h = tb.hopt ? (tb.W + 63) / 64 : 0;  // H of the saving sweep: every chunk
+            int32_t n_chunks_h = 0;  // H of the saving sweep: the chunks below the largest msaH
+            if (tb.hopt) {
+                int32_t sat_h = 0;
+                for (int32_t s = 0; s < ch.L - d; ++s)
+                    sat_h = max(sat_h, ch.h_msaH[row_of(ch.L, s, min(s + d + BAND - 1, ch.L - 1))]);
+                n_chunks_h = min((tb.W + 63) / 64, run_chunks(sat_h));
+            }
             prof->work[KFILL_PRODUCT] += product_work(ch.L, tb.W, d, BAND, 0, d, 0, d) * (tb.hopt ? 2 : 1);
             const int32_t n_rb = (ch.L - d + SW - 1) / SW;  // row blocks: a workgroup holds SW rows
             const bool cnt = tb.ctr != nullptr;
@@ -1212,8 +1230,15 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
         for (int32_t s = 0; s + d < ch.L; ++s) sat = max(sat, ch.h_msa[row_of(ch.L, s, s + d)]);
         const int32_t n_run = (int32_t)std::min<int64_t>(fin_x, ((int64_t)sat + FC - 1) / FC);
         const int32_t fin_h = tb.hopt && d >= 1 ? fin_x : 0;  // H(s, s+d) of the saving sweep
+        int32_t n_run_h = 0;  // H's chunks from n_run_h on lie past every cell's msaH: they only store
+        if (fin_h) {
+            int32_t sat_h = 0;
+            for (int32_t s = 0; s + d < ch.L; ++s) sat_h = max(sat_h, ch.h_msaH[row_of(ch.L, s, s + d)]);
+            n_run_h = (int32_t)std::min<int64_t>(fin_x, ((int64_t)sat_h + FC - 1) / FC);
+        }
         e = launch(prof, KFILL_FINALIZE, tb.ctr ? k_finalize<true> : k_finalize<false>,
-                   dim3(chunk_grid(fin_x + fin_h, ch.L - d)), dim3(FT), stream, ch, tb, d, midmin, fin_x, n_run, fin_h);
+                   dim3(chunk_grid(fin_x + fin_h, ch.L - d)), dim3(FT), stream, ch, tb, d, midmin, fin_x, n_run, fin_h,
+                   n_run_h);
         if (e != hipSuccess) return e;
         ++n;
         const int32_t D = (d / midmin) * midmin, near = D > 0 ? 2 * (d - D) : d;
@@ -1230,12 +1255,12 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
             // stored partial and the H row written.
             for (int32_t s = 0; s + d < ch.L; ++s) {
                 const int64_t run = std::min<int64_t>(tb.W, (int64_t)n_run * FC);
-                prof->eval[KFILL_FINALIZE] += run * (near + ch.K + (tb.hopt && d >= 2 ? ch.K : 0)) +
-                                              (tb.hopt ? (int64_t)tb.W * near : 0);
+                const int64_t run_h = std::min<int64_t>(tb.W, (int64_t)n_run_h * FC);
+                prof->eval[KFILL_FINALIZE] += run * (near + ch.K + (tb.hopt && d >= 2 ? ch.K : 0)) + run_h * near;
                 prof->bytes[KFILL_FINALIZE] +=
                     (run * (2 * near + (D > 0) + (d > 0) + 1) + (tb.W - run) + tb.W +
                      (s + d + 1 < ch.L ? (int64_t)tb.W * (tb.aq ? 2 : 1) : 0) +
-                     (fin_h ? (int64_t)tb.W * (2 * near + (D > 0) + 1) : 0)) * 4;
+                     (fin_h ? run_h * (2 * near + (D > 0)) + tb.W : 0)) * 4;
             }
         }
     }
