@@ -18,7 +18,7 @@ import numpy as np
 
 import oracle
 from oracle import brute
-from paper_2307_01236_amd.chaingen import Chain, make_random_chain, with_refwd
+from paper_2307_01236_amd.chaingen import Chain, make_random_chain, store_all_bound, with_refwd
 
 INF = oracle.INF
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -235,3 +235,34 @@ def test_simulator_rejects_refwd_without_kept_data():
     ops = np.array([(KIND[k], b, o) for k, b, o in g["schedule_at_M8"]["ops"]], dtype=np.int32)
     ok, _, _, idx = oracle.simulate(plain, ops)  # no re-forward times: the op is illegal
     assert not ok and ops[idx, 0] == oracle.REFWD
+
+
+def test_h_store_all_regime():
+    """Every candidate of H(s,t,u) (t > s) costs at least its sweep time P(s,i) plus
+    lb(s,i-1) + lb(i,t) = lb(s,t), so H >= lb(s,t) + r(F_s^0); split s+1 reaches that once
+    its sweep fits (x_s + x_{s+1} + tmp(F_s^0) <= u) and both of its parts are at their lb,
+    Opt(s,s,u - x_s) = lb(s,s) and Opt(s+1,t,u - x_{s+1}) = lb(s+1,t).  The thresholds come
+    from the oracle's own Opt rows (the first budget from which a row stays at its lb)."""
+    for ch in mid_sweep_chains():
+        M = store_all_bound(ch) * 2
+        sol = oracle.solve(ch, M)
+        L = ch.L
+        c1 = (ch.fwd.astype(np.int64) + ch.bwd).min(axis=1)
+        lb = lambda s, t: int(c1[s:t + 1].sum())
+
+        def msa(s, t):  # the first budget from which Opt(s,t,.) stays at lb(s,t)
+            row = sol.opt_row(s, t).astype(np.int64)
+            at = np.nonzero(row != lb(s, t))[0]
+            return 0 if len(at) == 0 else int(at[-1]) + 1
+
+        hv = sol.hval.astype(np.int64)
+        for s in range(L - 1):
+            for t in range(s + 1, L):
+                bound = lb(s, t) + int(ch.fn_time[s])
+                h = hv[:, oracle.cell(L, s, t)]
+                fin = h[h != INF]
+                assert (fin >= bound).all(), (ch.name, s, t)
+                u0 = max(int(ch.x[s]) + int(ch.x[s + 1]) + int(ch.fn_tmp[s]), msa(s, s) + int(ch.x[s]),
+                         msa(s + 1, t) + int(ch.x[s + 1]))
+                assert u0 <= M, (ch.name, s, t, u0)
+                assert (h[u0:] == bound).all(), (ch.name, s, t, u0)
