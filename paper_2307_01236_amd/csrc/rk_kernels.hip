@@ -776,6 +776,12 @@ __device__ inline int32_t ldrow(const int32_t *base, uint32_t pitch, uint32_t by
     return __builtin_amdgcn_raw_buffer_load_b32(r, (int)byte_off, 0, 0);
 }
 
+// A store marked nontemporal: its line is the first the caches let go.  The finalize writes
+// several rows per cell that only later launches read, most of them on other XCDs; with
+// these stores so marked the fill measured 0.13 ms faster (0.33 ms with the saving sweep),
+// the products and mids included, which keep more of their operands in L2.
+__device__ inline void st_nt(int32_t v, int32_t *p) { __builtin_nontemporal_store(v, p); }
+
 template <bool CNT>
 __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t d, int32_t midmin,
                                                  int32_t n_chunks, int32_t n_run, int32_t n_chunks_h,
@@ -975,7 +981,7 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
             const int32_t m = ml + 64 * c;
-            if (m < W) hrow[m] = min(best[c], DINF);
+            if (m < W) st_nt(min(best[c], DINF), &hrow[m]);
         }
         return;
     }
@@ -991,17 +997,17 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
     for (int c = 0; c < NC; ++c) {
         const int32_t m = ml + 64 * c;
         if (m < padl) {  // keep the left pads infinite
-            orow[m - padl] = DINF;
-            if (qrow) qrow[m - padl] = DINF;
+            st_nt(DINF, &orow[m - padl]);
+            if (qrow) st_nt(DINF, &qrow[m - padl]);
         }
         if (m < W) {
             const int32_t v = min(best[c], DINF);
-            orow[m] = v;
-            if (m < xs) srow[m] = DINF;
-            if ((int64_t)m + xs < W) srow[m + xs] = v;
+            st_nt(v, &orow[m]);
+            if (m < xs) st_nt(DINF, &srow[m]);
+            if ((int64_t)m + xs < W) st_nt(v, &srow[m + xs]);
             if (t + 1 < L) {
-                arow[m] = m >= need2 ? min(P + v, DINF) : DINF;
-                if (qrow) qrow[m] = m + xs >= need3 ? min(P + v, DINF) : DINF;
+                st_nt(m >= need2 ? min(P + v, DINF) : DINF, &arow[m]);
+                if (qrow) st_nt(m + xs >= need3 ? min(P + v, DINF) : DINF, &qrow[m]);
             }
         }
     }
