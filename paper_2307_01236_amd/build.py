@@ -21,6 +21,9 @@ HIPCC_FLAGS = [
     "-Wall", "-Wno-unused-command-line-argument",
     # keep the compiler from emitting packed fp32 instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # preload a kernel's leading scalar arguments into SGPRs at wave start (as many as fit;
+    # none for kernels whose first argument is a struct); the finalize is laid out for it
+    "-mllvm", "-amdgpu-kernarg-preload-count=16",
 ]
 
 

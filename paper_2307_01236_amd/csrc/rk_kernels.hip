@@ -782,21 +782,32 @@ __device__ inline int32_t ldrow(const int32_t *base, uint32_t pitch, uint32_t by
 // the products and mids included, which keep more of their operands in L2.
 __device__ inline void st_nt(int32_t v, int32_t *p) { __builtin_nontemporal_store(v, p); }
 
+// The arguments before the first aggregate are preloaded into SGPRs when a wave starts (the
+// library is built with kernarg preloading of up to 14 dwords): the three table pointers and
+// the scalars that the first table loads depend on, so that a wave issues those loads without
+// waiting on a kernel-argument load first (fill 10.37 -> 10.17 ms, 384 launches).  dpack
+// holds d, D = d rounded down to a multiple of the narrowest mid width (bits 11..21), whether
+// the chain has the saving sweep (bit 22) and the case-1 halo min(xbar_halo, 511) (bits
+// 23..31); n_tot = n_chunks plus H's chunks.  The other operands come from ch and tb.
+static_assert(RK_MAX_L < 2048, "span lengths are packed in 11 bits");
 template <bool CNT>
-__global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t d, int32_t midmin,
-                                                 int32_t n_chunks, int32_t n_run, int32_t n_chunks_h,
-                                                 int32_t n_run_h)
+__global__ __launch_bounds__(FT) void k_finalize(int32_t *p_opt, int32_t *p_os, int32_t *p_ap, uint32_t dpack,
+                                                 int32_t n_tot, int32_t n_chunks, int32_t n_run, int32_t L,
+                                                 int32_t W, int32_t padl, int32_t stride32, DevChain ch,
+                                                 Tables tb, int32_t n_run_h)
 {
     constexpr int32_t FB = 8, NC = FC / FT, NST = (HMAX + FC) / FT;
     __shared__ int32_t seg[HMAX + FC], seg3[HMAX + FC];
-    const int32_t L = ch.L, K = ch.K, W = tb.W;
+    const int32_t K = ch.K;
+    const int32_t d = (int32_t)(dpack & 0x7ffu);
+    const int32_t D = (int32_t)((dpack >> 11) & 0x7ffu);  // the products cover splits with max(a, b) < D
     // Tiles of one column chunk are adjacent in row s, and adjacent tiles run on one XCD: the
     // case-1 row (s+1, t) of a cell was written in the previous launch by the workgroup of
     // the neighbouring tile, so it is often still in that XCD's L2 (rows adjacent: 5.95 ms a
     // fill, column chunks adjacent: 6.15 ms, no XCD-aware order: 6.7 ms).
     int32_t chunk, s;
     chunk_tile(blockIdx.x, (uint32_t)(L - d), &chunk, &s);
-    if (chunk >= n_chunks + n_chunks_h) return;
+    if (chunk >= n_tot) return;
     // chunks from n_chunks on finish H(s, t) of the saving sweep instead of Opt(s, t)
     const bool hp = chunk >= n_chunks;
     if (hp) chunk -= n_chunks;
@@ -806,12 +817,10 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
     const int32_t wave = __builtin_amdgcn_readfirstlane((int32_t)(threadIdx.x >> 6));
     const int32_t m0 = mbase + 64 * NC * wave;  // the wave's first column
     const int32_t ml = m0 + lane;           // column c of the lane: ml + 64 c
-    const int64_t stride = tb.stride;
+    const int64_t stride = stride32;
     const uint32_t pitch = (uint32_t)stride * 4u;
-    const int32_t padl = tb.padl;
     const int64_t row_st = row_of(L, s, t);
-    int32_t *const orow = tb.opt + row_st * stride + padl;  // column 0
-    const int32_t D = (d / midmin) * midmin;  // the products cover splits with max(a, b) < D
+    int32_t *const orow = p_opt + row_st * stride + padl;  // column 0
     const int32_t ip = t + 1 < L ? s * L + t + 1 : 0;
     // per-lane column offsets (past the last budget: the last one, computed and not stored)
     uint32_t col[NC];  // byte offsets
@@ -825,7 +834,7 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
     int32_t best[NC];
     auto splits = [&](const int32_t *ltab, int32_t lsh, int32_t i0, int32_t n) {
         const int32_t *pa = ltab + (row_of(L, s, s) + (i0 - 1 - s)) * stride + padl - lsh;
-        const int32_t *pq = tb.os + row_of(L, i0, t) * stride + padl;
+        const int32_t *pq = p_os + row_of(L, i0, t) * stride + padl;
         int32_t i = i0;
         for (int32_t j0 = 0; j0 < n; j0 += FB) {
             int32_t va[FB][NC], vq[FB][NC];
@@ -897,10 +906,10 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
     } else {
         // the case-1 row Opt(s+1, t) and, with the saving sweep, the row H(s+1, t) of case 3,
         // staged: column mbase - H + q at seg[q] (seg3[q])
-        const int32_t H = ch.xbar_halo;
+        const int32_t H = (int32_t)(dpack >> 23);
         const bool staged = d > 0 && H <= HMAX;
-        const bool sweep = ch.c3 != nullptr && d >= 2;
-        const int32_t *const rest = d > 0 ? tb.opt + row_of(L, s + 1, t) * stride + padl : nullptr;
+        const bool sweep = (dpack >> 22 & 1u) && d >= 2;
+        const int32_t *const rest = d > 0 ? p_opt + row_of(L, s + 1, t) * stride + padl : nullptr;
         const int32_t *const hrest = sweep ? tb.hopt + row_of(L, s + 1, t) * stride + padl : nullptr;
         int32_t stv[NST], stv3[NST];
         if (staged) {
@@ -914,7 +923,7 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
         }
 #pragma unroll
         for (int c = 0; c < NC; ++c) best[c] = D > 0 ? ldb(orow, col[c]) : DINF;
-        near_first(tb.ap, 0);
+        near_first(p_ap, 0);
 
         // case 1, option o: r(F_s^o) + r(B_s^o) + Opt(s+1,t,m-xbar), valid iff m >= need1[s][o];
         // case 3 (the saving sweep), option o: r(F)+r(B)+refwd + H(s+1,t,m-mem), same validity
@@ -972,7 +981,7 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
                         if (ml + 64 * c >= need1[o])
                             best[c] = min(best[c], c3[o] + ldb(hrest - (xbar[o] - x1), col[c]));
         }
-        near_second(tb.ap, 0);  // after case 1 and case 3, whose minima tighten the bound test
+        near_second(p_ap, 0);  // after case 1 and case 3, whose minima tighten the bound test
     }
 
     // stores last: until here every scalar operand may come from the scalar cache
@@ -988,8 +997,8 @@ __global__ __launch_bounds__(FT) void k_finalize(DevChain ch, Tables tb, int32_t
     // Opt, its copy in the right operand table (Opt(s, t, m) at column m + x_s, infinity
     // below x_s), the left operand ap(s, t+1) of Eq. fn and, with the saving sweep, the left
     // operand aq(s, t+1, v) = P[s][t+1] + Opt(s, t, v) of H(s, .) if the sweep s..t fits v + x_s
-    int32_t *const srow = tb.os + row_st * stride + padl;
-    int32_t *const arow = tb.ap + row_st * stride + padl;
+    int32_t *const srow = p_os + row_st * stride + padl;
+    int32_t *const arow = p_ap + row_st * stride + padl;
     int32_t *const qrow = tb.aq ? tb.aq + row_st * stride + padl : nullptr;
     const int32_t need2 = t + 1 < L ? ch.need2[ip] : 0, P = t + 1 < L ? ch.P[ip] : 0;
     const int32_t need3 = qrow && t + 1 < L ? ch.need3[ip] : 0, xs = ch.x[s];
@@ -1242,9 +1251,11 @@ hipError_t launch_fill(const DevChain &ch, const Tables &tb, hipStream_t stream,
             for (int32_t s = 0; s + d < ch.L; ++s) sat_h = max(sat_h, ch.h_msaH[row_of(ch.L, s, s + d)]);
             n_run_h = (int32_t)std::min<int64_t>(fin_x, ((int64_t)sat_h + FC - 1) / FC);
         }
+        const uint32_t dpack = (uint32_t)d | (uint32_t)(d / midmin * midmin) << 11 |
+                               (uint32_t)(ch.c3 != nullptr) << 22 | (uint32_t)std::min(ch.xbar_halo, 511) << 23;
         e = launch(prof, KFILL_FINALIZE, tb.ctr ? k_finalize<true> : k_finalize<false>,
-                   dim3(chunk_grid(fin_x + fin_h, ch.L - d)), dim3(FT), stream, ch, tb, d, midmin, fin_x, n_run, fin_h,
-                   n_run_h);
+                   dim3(chunk_grid(fin_x + fin_h, ch.L - d)), dim3(FT), stream, tb.opt, tb.os, tb.ap, dpack,
+                   fin_x + fin_h, fin_x, n_run, ch.L, tb.W, tb.padl, (int32_t)tb.stride, ch, tb, n_run_h);
         if (e != hipSuccess) return e;
         ++n;
         const int32_t D = (d / midmin) * midmin, near = D > 0 ? 2 * (d - D) : d;
