@@ -885,44 +885,45 @@ __global__ __launch_bounds__(FT) void k_finalize(int32_t *p_opt, int32_t *p_os, 
     // store.  The products and mids of these spans ran on at least the chunks below n_run.
     // (The stores stay after every load on every path, so the loads of the per-block and
     // per-option arrays may use the scalar cache.)
-    if (hp && chunk >= n_run_h) {
-        // past msaH(s,t) of every cell of the diagonal: H(s,t) = lb(s,t) + P[s][s+1] (the
-        // lower bound of every candidate, reached by split s+1); the products did not run here
-        const int32_t hv = ch.lb[row_st] + ch.P[(int64_t)s * L + s + 1];
+    // Opt below msa (the main path): the case-1 row Opt(s+1, t), staged (column mbase - H + q
+    // at seg[q]), and the products' partial are loaded first, before anything that waits on a
+    // kernel-argument load: their addresses need only the preloaded arguments.  Opt's paths
+    // come first for the same reason.
+    const bool main_path = !hp && chunk < n_run;
+    const int32_t H = (int32_t)(dpack >> 23);
+    const bool staged = main_path && d > 0 && H <= HMAX;
+    int32_t stv[NST];
+    if (staged) {
+        const int32_t *const rrow = p_opt + row_of(L, s + 1, t) * stride;  // column -padl
 #pragma unroll
-        for (int c = 0; c < NC; ++c) best[c] = hv;
-    } else if (hp) {
-        // H(s, t) = min_i aq(s, i, m - x_s) + Opt(i, t, m - x_i): the products' partial, then
-        // the near splits
-        const int32_t *const hrow = tb.hopt + row_st * stride + padl;
+        for (int k = 0; k < NST; ++k) {
+            const int32_t q = (int32_t)threadIdx.x + FT * k, c = mbase - H + q;
+            // columns left of the row's pad are set to infinity when the row is staged
+            stv[k] = ldrow(rrow, pitch, q < H + FC && c >= -padl ? (uint32_t)(c + padl) * 4u : OOB);
+        }
+    }
+    if (main_path) {
 #pragma unroll
-        for (int c = 0; c < NC; ++c) best[c] = D > 0 ? ldb(hrow, col[c]) : DINF;
-        near_first(tb.aq, min(ch.x[s], padl));
-        near_second(tb.aq, min(ch.x[s], padl));
-    } else if (chunk >= n_run) {
+        for (int c = 0; c < NC; ++c) best[c] = D > 0 ? ldb(orow, col[c]) : DINF;
+    }
+    if (!hp && chunk >= n_run) {
         const int32_t lbv = ch.lb[row_st];
 #pragma unroll
         for (int c = 0; c < NC; ++c) best[c] = lbv;
-    } else {
-        // the case-1 row Opt(s+1, t) and, with the saving sweep, the row H(s+1, t) of case 3,
-        // staged: column mbase - H + q at seg[q] (seg3[q])
-        const int32_t H = (int32_t)(dpack >> 23);
-        const bool staged = d > 0 && H <= HMAX;
+    } else if (!hp) {
+        // with the saving sweep, the row H(s+1, t) of case 3, staged the same way (seg3)
         const bool sweep = (dpack >> 22 & 1u) && d >= 2;
         const int32_t *const rest = d > 0 ? p_opt + row_of(L, s + 1, t) * stride + padl : nullptr;
         const int32_t *const hrest = sweep ? tb.hopt + row_of(L, s + 1, t) * stride + padl : nullptr;
-        int32_t stv[NST], stv3[NST];
-        if (staged) {
+        int32_t stv3[NST];
+        if (staged && sweep) {
 #pragma unroll
             for (int k = 0; k < NST; ++k) {
                 const int32_t q = (int32_t)threadIdx.x + FT * k, c = mbase - H + q;
-                stv[k] = q < H + FC && c >= -padl ? rest[c] : DINF;
                 // H is read at m - mem >= 0 only (need1 >= mem): columns below 0 are never used
-                stv3[k] = sweep && q < H + FC && c >= 0 ? hrest[c] : DINF;
+                stv3[k] = q < H + FC && c >= 0 ? hrest[c] : DINF;
             }
         }
-#pragma unroll
-        for (int c = 0; c < NC; ++c) best[c] = D > 0 ? ldb(orow, col[c]) : DINF;
         near_first(p_ap, 0);
 
         // case 1, option o: r(F_s^o) + r(B_s^o) + Opt(s+1,t,m-xbar), valid iff m >= need1[s][o];
@@ -940,7 +941,7 @@ __global__ __launch_bounds__(FT) void k_finalize(int32_t *p_opt, int32_t *p_os, 
             for (int k = 0; k < NST; ++k) {
                 const int32_t q = (int32_t)threadIdx.x + FT * k;
                 if (q < H + FC) {
-                    seg[q] = stv[k];
+                    seg[q] = mbase - H + q >= -padl ? stv[k] : DINF;
                     if (sweep) seg3[q] = stv3[k];
                 }
             }
@@ -982,6 +983,20 @@ __global__ __launch_bounds__(FT) void k_finalize(int32_t *p_opt, int32_t *p_os, 
                             best[c] = min(best[c], c3[o] + ldb(hrest - (xbar[o] - x1), col[c]));
         }
         near_second(p_ap, 0);  // after case 1 and case 3, whose minima tighten the bound test
+    } else if (chunk >= n_run_h) {
+        // past msaH(s,t) of every cell of the diagonal: H(s,t) = lb(s,t) + P[s][s+1] (the
+        // lower bound of every candidate, reached by split s+1); the products did not run here
+        const int32_t hv = ch.lb[row_st] + ch.P[(int64_t)s * L + s + 1];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) best[c] = hv;
+    } else {
+        // H(s, t) = min_i aq(s, i, m - x_s) + Opt(i, t, m - x_i): the products' partial, then
+        // the near splits
+        const int32_t *const hrow = tb.hopt + row_st * stride + padl;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) best[c] = D > 0 ? ldb(hrow, col[c]) : DINF;
+        near_first(tb.aq, min(ch.x[s], padl));
+        near_second(tb.aq, min(ch.x[s], padl));
     }
 
     // stores last: until here every scalar operand may come from the scalar cache
