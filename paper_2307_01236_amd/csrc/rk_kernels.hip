@@ -905,6 +905,7 @@ __global__ __launch_bounds__(FT) void k_finalize(int32_t *p_opt, int32_t *p_os, 
     if (main_path) {
 #pragma unroll
         for (int c = 0; c < NC; ++c) best[c] = D > 0 ? ldb(orow, col[c]) : DINF;
+        near_first(p_ap, 0);
     }
     if (!hp && chunk >= n_run) {
         const int32_t lbv = ch.lb[row_st];
@@ -924,7 +925,6 @@ __global__ __launch_bounds__(FT) void k_finalize(int32_t *p_opt, int32_t *p_os, 
                 stv3[k] = q < H + FC && c >= 0 ? hrest[c] : DINF;
             }
         }
-        near_first(p_ap, 0);
 
         // case 1, option o: r(F_s^o) + r(B_s^o) + Opt(s+1,t,m-xbar), valid iff m >= need1[s][o];
         // case 3 (the saving sweep), option o: r(F)+r(B)+refwd + H(s+1,t,m-mem), same validity
