@@ -1497,7 +1497,8 @@ __global__ __launch_bounds__(64) void k_backtrace(DevChain ch, Tables tb, int32_
         // (L <= 2000), so each address is one 32x32+64 multiply-add from the table base.
         uint64_t best = ~0ull;
         auto take = [&](bool ok, uint32_t v, uint32_t code) {
-            best = min(best, ok ? ((uint64_t)v << 32) | code : ~0ull);
+            const uint64_t key = ok ? ((uint64_t)v << 32) | code : ~0ull;
+            best = key < best ? key : best;
         };
         auto row32 = [&](int32_t a, int32_t b) { return (uint32_t)(a * L - ((a * (a - 1)) >> 1) + b - a); };
         const uint32_t ustride = (uint32_t)stride;
