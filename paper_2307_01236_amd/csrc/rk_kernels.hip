@@ -928,9 +928,9 @@ __global__ __launch_bounds__(FT) void k_finalize(int32_t *p_opt, int32_t *p_os, 
     // (The stores stay after every load on every path, so the loads of the per-block and
     // per-option arrays may use the scalar cache.)
     // Opt below msa (the main path): the case-1 row Opt(s+1, t), staged (column mbase - H + q
-    // at seg[q]), and the products' partial are loaded first, before anything that waits on a
-    // kernel-argument load: their addresses need only the preloaded arguments.  Opt's paths
-    // come first for the same reason.
+    // at seg[q]), the products' partial and the first near range are loaded first, before
+    // anything that waits on a kernel-argument load: their addresses need only the preloaded
+    // arguments.  Opt's paths come first for the same reason.
     const bool main_path = !hp && chunk < n_run;
     const int32_t H = (int32_t)(dpack >> 23);
     const bool staged = main_path && d > 0 && H <= HMAX;
