@@ -730,17 +730,32 @@ __device__ __attribute__((always_inline)) inline bool mid_tile(const DevChain &c
 // chunk by column chunk (group A's row blocks, then group B's), and consecutive tiles run
 // on one XCD: each XCD keeps the same range of columns as in the finalize launches, whose
 // recent rows the mids read.
+// The arguments before ch are preloaded into SGPRs when a wave starts, as for the finalize:
+// the table pointers and the scalars that the tile's first loads need (tau in bits 0..10 of
+// tpack, the fold flag in bit 11; n_tot = n_chunks plus H's chunks).  They stand in for the
+// same fields of ch and tb (fill 9.92 -> 9.90 ms).
 template <int WD, bool LO0, bool CNT>
-__global__ __launch_bounds__(64) void k_mid(DevChain ch, Tables tb, int32_t tau, int32_t accumulate,
-                                            int32_t n_chunks, int32_t n_chunks_h)
+__global__ __launch_bounds__(64) void k_mid(int32_t *p_opt, int32_t *p_os, int32_t *p_ap, int32_t stride32,
+                                            int32_t padl, int32_t W, int32_t L, int32_t inf_row, uint32_t tpack,
+                                            int32_t n_tot, int32_t n_chunks, DevChain ch, Tables tb,
+                                            int32_t n_chunks_h)
 {
+    const int32_t tau = (int32_t)(tpack & 0x7ffu), accumulate = (int32_t)(tpack >> 11);
+    tb.opt = p_opt;
+    tb.os = p_os;
+    tb.ap = p_ap;
+    tb.stride = stride32;
+    tb.padl = padl;
+    tb.W = W;
+    tb.inf_row = inf_row;
+    ch.L = L;
     constexpr int R = mid_rows<WD>();
     const int32_t n_blk = (ch.L - tau + R - 1) / R;
     // per column chunk: group A's n_blk tiles, then group B's (lo > 0); gi indexes the group.
     // Chunks from n_chunks on are H's (the saving sweep).
     int32_t mc, rem;
     chunk_tile(blockIdx.x, (LO0 ? 1 : 2) * n_blk, &mc, &rem);
-    if (mc >= n_chunks + n_chunks_h) return;
+    if (mc >= n_tot) return;
     const bool hp = mc >= n_chunks;
     if (hp) mc -= n_chunks;
     const int32_t gi = mc * n_blk + rem % n_blk;
@@ -1205,10 +1220,13 @@ static hipError_t launch_mid(const DevChain &ch, const Tables &tb, hipStream_t s
         if ((e = prof->records(stream, n_rec)) != hipSuccess) return e;
         tr.rec = prof->d_rec;
     }
+    const uint32_t tpack = (uint32_t)d | (uint32_t)(lo > 0) << 11;  // d < 2048
     e = lo == 0 ? launch(prof, KFILL_MID, cnt ? k_mid<WD, true, true> : k_mid<WD, true, false>, grid, dim3(64),
-                         stream, ch, tr, d, 0, n_chunks, n_chunks_h)
+                         stream, tr.opt, tr.os, tr.ap, (int32_t)tr.stride, tr.padl, tr.W, ch.L, (int32_t)tr.inf_row,
+                         tpack, n_chunks + n_chunks_h, n_chunks, ch, tr, n_chunks_h)
                 : launch(prof, KFILL_MID, cnt ? k_mid<WD, false, true> : k_mid<WD, false, false>, grid, dim3(64),
-                         stream, ch, tr, d, 1, n_chunks, n_chunks_h);
+                         stream, tr.opt, tr.os, tr.ap, (int32_t)tr.stride, tr.padl, tr.W, ch.L, (int32_t)tr.inf_row,
+                         tpack, n_chunks + n_chunks_h, n_chunks, ch, tr, n_chunks_h);
     if (e != hipSuccess) return e;
     ++*n;
     if (prof->on) {
